@@ -1,0 +1,267 @@
+"""CPU oracle for the AdaPLD draft-and-verify step (test infrastructure only).
+
+This module is a plain, slow, float64 statement of what one decoding iteration
+of AdaPLD computes between the target model's forward passes.  It exists to
+check the HIP path: only the test suite, the package smoke check and the
+benchmark's CPU-baseline leg may import it.  It shares no code with the HIP
+path and imports nothing from it; its inputs are plain NumPy arrays (bf16
+values arrive as their uint16 bit patterns and are decoded here, exactly, to
+float64).
+
+Four steps, per sequence, in the paper's order (Sec. 3.3 - 3.6, Algorithm 1):
+
+``lexical_match``   -- lexical anchoring (Sec. 3.3, the exact-match set), read
+                       as a longest-suffix n-gram match, n = n_max .. 1.
+``semantic_topk``   -- the lexical/semantic backoff (Sec. 3.3) and the
+                       hidden-state reranking (Sec. 3.4): cosine scores, ranked
+                       by (score desc, position asc), top k kept.
+``build_draft_tree``-- reuse construction (Sec. 3.5) organised as a draft tree
+                       (Sec. 3.6): one branch per distinct successor token,
+                       each a copied span; an ancestor-or-self mask.
+``tree_verify_attn``-- tree-masked attention over the KV cache (Sec. 3.6,
+                       tree attention after Medusa), softmax in float64.
+
+Readings of the paper used here (where it is silent, ambiguous or where the
+reproduced workload differs from its text):
+
+* positions are 0-based; candidates j lie in [n-1, L-2], so every candidate
+  has a following token (Sec. 3.3 uses 1 <= j < |M|);
+* only the longest non-empty n-gram level is kept (n_max = 1 is exactly the
+  paper's single-token match);
+* the semantic score is the cosine between bank rows and an explicit query
+  vector (by default the bank row of the last position), over candidate rows
+  r (lexical hit) or all rows [0, L-2] (fallback); a zero norm gives cosine 0;
+* tau, when given, filters fallback scores below it; it never filters a
+  lexical hit;
+* branch tokens are the first W distinct successor tokens M[r+1] along the
+  ranked list; each branch is M[r+1 .. min(r+1+S, L-1)] (the branch token
+  followed by up to S copied tokens).  With a lexical hit, branch 0 is the
+  paper's main copy path with maximum copy length S+1;
+* the tree is stored branch-major, depth-major within a branch; the parent of
+  a depth-0 node is -1 (the root, the last context token, lives in the KV
+  cache and is not a query row);
+* verification keys for node u are all context keys 0..L-1 followed by the
+  tree keys of u's ancestors-or-self in ascending node order.
+
+Parity unpinned: none of the paper's printed numbers can pin these functions
+(the paper prints no worked example); every function is pinned by brute force,
+library routines, closed forms and invariants in the test suite instead.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+KIND_NONE = 0
+KIND_LEX = 1
+KIND_SEM = 2
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Exact decode of bf16 bit patterns (uint16) to float64."""
+    b = np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+# --------------------------------------------------------------------------
+# Step 1: lexical anchoring (Sec. 3.3, exact-match candidate set; Alg. 1 ExactMatch)
+# --------------------------------------------------------------------------
+
+def lexical_match(tokens: np.ndarray, n_max: int):
+    """Longest-suffix n-gram candidates of one context.
+
+    For n = n_max down to 1, C_n holds every j in [n-1, L-2] whose n tokens
+    ending at j equal the last n tokens of the context.  The first non-empty
+    level wins.  Returns (n_star, C) with C ascending; (0, []) when no level
+    has a candidate.
+    """
+    M = np.asarray(tokens)
+    L = int(M.shape[0])
+    assert n_max >= 1
+    for n in range(n_max, 0, -1):
+        if L < n + 1:
+            continue
+        js = np.arange(n - 1, L - 1)
+        hit = np.ones(js.shape[0], dtype=bool)
+        for i in range(n):
+            hit &= M[js - i] == M[L - 1 - i]
+        C = js[hit]
+        if C.size > 0:
+            return n, [int(j) for j in C]
+    return 0, []
+
+
+# --------------------------------------------------------------------------
+# Step 2: backoff + hidden-state reranking (Sec. 3.3 backoff rule; Sec. 3.4 scores)
+# --------------------------------------------------------------------------
+
+def cosine_rows(H: np.ndarray, rows, q: np.ndarray) -> np.ndarray:
+    """cos(H[r], q) for r in rows, float64; 0 where either norm is 0."""
+    rows = np.asarray(rows, dtype=np.int64)
+    X = H[rows]
+    dots = X @ q
+    nx = np.sqrt(np.einsum("ij,ij->i", X, X))
+    nq = np.sqrt(q @ q)
+    den = nx * nq
+    out = np.zeros(rows.shape[0], dtype=np.float64)
+    ok = den > 0
+    out[ok] = dots[ok] / den[ok]
+    return out
+
+
+def semantic_topk(bank: np.ndarray, query, cand, k: int, tau=None):
+    """Rank the retrieval candidates of one sequence.
+
+    bank: (L, d) float64 hidden states; query: (d,) float64 or None, meaning
+    the last bank row.  cand: the lexical candidate list (possibly empty).
+    With candidates (a lexical hit) the scored rows are the candidates and
+    kind = LEX; otherwise every row in [0, L-2] is scored (semantic fallback),
+    entries below tau are dropped when tau is given, and kind = SEM if any
+    entry remains, else NONE.  Ranking: score descending, then position
+    ascending; the first min(k, #rows) are kept.
+    Returns (kind, positions, scores).
+    """
+    L = int(bank.shape[0])
+    q = bank[L - 1] if query is None else np.asarray(query, dtype=np.float64)
+    if len(cand) > 0:
+        rows = np.asarray(cand, dtype=np.int64)
+        lexical = True
+    else:
+        rows = np.arange(0, max(L - 1, 0), dtype=np.int64)
+        lexical = False
+    if rows.size == 0:
+        return KIND_NONE, [], []
+    s = cosine_rows(bank, rows, q)
+    order = np.lexsort((rows, -s))
+    top = order[: min(k, rows.size)]
+    pos = [int(rows[i]) for i in top]
+    sc = [float(s[i]) for i in top]
+    if lexical:
+        return KIND_LEX, pos, sc
+    if tau is not None:
+        keep = [i for i in range(len(sc)) if sc[i] >= tau]
+        pos = [pos[i] for i in keep]
+        sc = [sc[i] for i in keep]
+    return (KIND_SEM if pos else KIND_NONE), pos, sc
+
+
+# --------------------------------------------------------------------------
+# Step 3: reuse construction as a draft tree (Sec. 3.5, Sec. 3.6; Alg. 1 BuildDraftTree)
+# --------------------------------------------------------------------------
+
+def build_draft_tree(tokens: np.ndarray, kind: int, ranked, W: int, S: int):
+    """Branches from the ranked retrieval list, as a tree.
+
+    Walks the ranked positions r in order; the successor token M[r+1] opens a
+    new branch unless an earlier branch already starts with it; at most W
+    branches.  A branch copies M[r+1 .. min(r+1+S, L-1)].  Returns a dict with
+    per-node lists token, parent, depth, src (the memory position the node
+    copies), the node count T, the branch list, and the (T, T) boolean
+    ancestor-or-self mask.
+    """
+    M = np.asarray(tokens)
+    L = int(M.shape[0])
+    branches = []
+    if kind != KIND_NONE:
+        used = set()
+        for r in ranked:
+            o = int(r) + 1
+            b = int(M[o])
+            if b in used:
+                continue
+            used.add(b)
+            branches.append(list(range(o, min(o + S, L - 1) + 1)))
+            if len(branches) == W:
+                break
+    token, parent, depth, src = [], [], [], []
+    for br in branches:
+        for dpt, p in enumerate(br):
+            u = len(token)
+            token.append(int(M[p]))
+            parent.append(-1 if dpt == 0 else u - 1)
+            depth.append(dpt)
+            src.append(p)
+    T = len(token)
+    mask = np.zeros((T, T), dtype=bool)
+    for u in range(T):
+        v = u
+        while v != -1:
+            mask[u, v] = True
+            v = parent[v]
+    return dict(token=token, parent=parent, depth=depth, src=src, T=T,
+                branches=branches, mask=mask)
+
+
+# --------------------------------------------------------------------------
+# Step 4: tree-masked verify attention (Sec. 3.6)
+# --------------------------------------------------------------------------
+
+def tree_verify_attn(Q, Kc, Vc, Kt, Vt, mask, L: int, scale: float):
+    """Attention of every tree node's query against context + ancestor keys.
+
+    Q: (T, Hq, D); Kc, Vc: (Hkv, >=L, D); Kt, Vt: (T, Hkv, D); mask: (T, T)
+    ancestor-or-self booleans; all float64.  Query head h reads kv head
+    h // (Hq // Hkv).  For node u the keys are Kc[g, 0..L-1] followed by
+    Kt[v, g] for every v with mask[u, v], v ascending; values likewise.
+    Returns O (T, Hq, D) and LSE (Hq, T) (natural log of the softmax
+    denominator of the scaled logits).
+    """
+    T, Hq, D = Q.shape
+    Hkv = Kc.shape[0]
+    G = Hq // Hkv
+    O = np.zeros((T, Hq, D), dtype=np.float64)
+    LSE = np.zeros((Hq, T), dtype=np.float64)
+    for u in range(T):
+        anc = [v for v in range(T) if mask[u, v]]
+        for g in range(Hkv):
+            keys = np.concatenate([Kc[g, :L], Kt[anc, g]], axis=0)
+            vals = np.concatenate([Vc[g, :L], Vt[anc, g]], axis=0)
+            heads = range(g * G, (g + 1) * G)
+            for h in heads:
+                z = scale * (keys @ Q[u, h])
+                m = z.max()
+                e = np.exp(z - m)
+                l = e.sum()
+                O[u, h] = (e @ vals) / l
+                LSE[h, u] = m + np.log(l)
+    return O, LSE
+
+
+# --------------------------------------------------------------------------
+# One whole step over a batch (Alg. 1, one loop iteration up to verification)
+# --------------------------------------------------------------------------
+
+def step(tokens, lens, bank_bits, query_bits, n_max, k, W, S, tau=None,
+         q_bits=None, kc_bits=None, vc_bits=None, kt_bits=None, vt_bits=None,
+         scale=None, seqs=None, verify=True):
+    """Run the four steps for the sequences in ``seqs`` (default: all).
+
+    tokens: (B, L_stride) int; lens: (B,); bank_bits: (B, L_stride, d) uint16;
+    query_bits: None (use row lens[b]-1) or (B, d) uint16.  Verify tensors are
+    bf16 bit patterns in the layouts Q (B, T_max, Hq, D), Kc/Vc
+    (B, Hkv, L_stride, D), Kt/Vt (B, T_max, Hkv, D).  Returns one dict per
+    sequence with every intermediate and output.
+    """
+    B = tokens.shape[0]
+    seqs = range(B) if seqs is None else seqs
+    out = []
+    for b in seqs:
+        L = int(lens[b])
+        M = np.asarray(tokens[b, :L])
+        n_star, C = lexical_match(M, n_max)
+        H = bf16_bits_to_f64(bank_bits[b, :L])
+        qv = None if query_bits is None else bf16_bits_to_f64(query_bits[b])
+        kind, pos, sc = semantic_topk(H, qv, C, k, tau)
+        tree = build_draft_tree(M, kind, pos, W, S)
+        rec = dict(b=b, n_star=n_star, cand=C, kind=kind, topk_pos=pos, topk_score=sc, tree=tree)
+        if verify and tree["T"] > 0:
+            T = tree["T"]
+            Q = bf16_bits_to_f64(q_bits[b, :T])
+            Kc = bf16_bits_to_f64(kc_bits[b, :, :L])
+            Vc = bf16_bits_to_f64(vc_bits[b, :, :L])
+            Kt = bf16_bits_to_f64(kt_bits[b, :T])
+            Vt = bf16_bits_to_f64(vt_bits[b, :T])
+            sc_ = (1.0 / np.sqrt(Q.shape[-1])) if scale is None else scale
+            O, LSE = tree_verify_attn(Q, Kc, Vc, Kt, Vt, tree["mask"], L, sc_)
+            rec.update(O=O, LSE=LSE)
+        out.append(rec)
+    return out

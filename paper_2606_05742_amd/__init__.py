@@ -1,0 +1,7 @@
+"""AdaPLD draft-and-verify hot path on MI355X (gfx950).
+
+The four steps of one decoding iteration run as hand-written HIP kernels
+behind the C-ABI library ``libadapld.so``; ``binding`` is a thin layer over
+it (argument marshalling only).  A missing library is an error, never a
+fallback.
+"""

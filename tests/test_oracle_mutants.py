@@ -1,0 +1,57 @@
+"""The oracle's pins catch plausible mistakes.
+
+Each mutant changes one spot of the oracle (a dropped term, an off-by-one, a
+wrong sign, a transposed operand, a wrong tie order) in a child process and
+runs the pin suite against it; every mutant must make the suite fail.
+"""
+import json
+import os
+import subprocess
+import sys
+
+from concurrent.futures import ThreadPoolExecutor
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+PINS = ["tests/test_oracle_lexical.py", "tests/test_oracle_semantic.py",
+        "tests/test_oracle_tree.py", "tests/test_oracle_verify.py"]
+
+MUTANTS = [
+    ("js = np.arange(n - 1, L - 1)", "js = np.arange(n - 1, L)"),              # anchor counts itself
+    ("js = np.arange(n - 1, L - 1)", "js = np.arange(n, L - 1)"),              # drops the first window
+    ("hit &= M[js - i] == M[L - 1 - i]", "hit &= M[js - i] == M[L - 2 - i]"),  # suffix off by one
+    ("for n in range(n_max, 0, -1):", "for n in range(1, n_max + 1):"),        # shortest level first
+    ("order = np.lexsort((rows, -s))", "order = np.lexsort((-rows, -s))"),    # ties to highest position
+    ("order = np.lexsort((rows, -s))", "order = np.lexsort((rows, s))"),      # ascending scores
+    ("nx = np.sqrt(np.einsum(\"ij,ij->i\", X, X))", "nx = np.einsum(\"ij,ij->i\", X, X)"),  # norm not rooted
+    ("rows = np.arange(0, max(L - 1, 0), dtype=np.int64)", "rows = np.arange(0, L, dtype=np.int64)"),  # query row scored
+    ("if sc[i] >= tau]", "if sc[i] > tau]"),                                   # tau boundary
+    ("    if lexical:\n        return KIND_LEX, pos, sc\n", "    if lexical:\n        pass\n"),  # tau applied to lexical hits
+    ("branches.append(list(range(o, min(o + S, L - 1) + 1)))", "branches.append(list(range(o, min(o + S, L - 1))))"),
+    ("            if b in used:\n                continue\n", "            pass\n"),            # no dedup
+    ("parent.append(-1 if dpt == 0 else u - 1)", "parent.append(-1)"),        # flat tree
+    ("            o = int(r) + 1\n", "            o = int(r)\n"),                # copies the anchor, not its successor
+    ("keys = np.concatenate([Kc[g, :L], Kt[anc, g]], axis=0)", "keys = np.concatenate([Kc[g, :L], Kt[:len(anc), g]], axis=0)"),
+    ("z = scale * (keys @ Q[u, h])", "z = (keys @ Q[u, h])"),                   # scale dropped
+    ("LSE[h, u] = m + np.log(l)", "LSE[h, u] = np.log(l)"),                   # max dropped
+    ("heads = range(g * G, (g + 1) * G)", "heads = range(g, Hq, Hkv)"),       # wrong GQA grouping
+    ("O[u, h] = (e @ vals) / l", "O[u, h] = (e @ vals)"),                       # no normalisation
+]
+
+
+def _run(mutant):
+    env = dict(os.environ, ADAPLD_ORACLE_MUTANT=json.dumps(list(mutant)))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", *PINS],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return r.returncode
+
+
+def test_pins_catch_every_mutant():
+    workers = max(1, min(8, len(os.sched_getaffinity(0))))
+    with ThreadPoolExecutor(workers) as ex:
+        codes = list(ex.map(_run, MUTANTS))
+    survivors = [m for m, c in zip(MUTANTS, codes) if c != 1]
+    assert not survivors, survivors
+
+
+def test_unmutated_oracle_passes_pins():
+    assert _run(("KIND_NONE = 0", "KIND_NONE = 0")) == 0
