@@ -1,0 +1,173 @@
+"""Benchmark of the AdaPLD draft-and-verify step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is the four library calls (lexical match, semantic top-k / rerank,
+draft tree, tree-masked verify attention) for every sequence of one batch of
+seeded synthetic inputs, with all inputs resident in HBM.  Two copies of the
+large inputs alternate between steps so that the 256 MB last-level cache
+cannot serve a step from the previous one.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(cfg, lens, cand_count, node_count):
+    """Bytes the method must move per step (each input read once, each output written once)."""
+    d, D, Hq, Hkv = cfg.d, cfg.D, cfg.Hq, cfg.Hkv
+    total = verify = scan = 0
+    for b in range(len(lens)):
+        L = int(lens[b])
+        T = int(node_count[b])
+        rows = int(cand_count[b]) if int(cand_count[b]) > 0 else max(L - 1, 0)
+        scan_b = 2 * d * rows + 2 * d                                   # scored rows + query
+        ver_b = 4 * Hkv * D * (L + T) + 4 * Hq * D * T + 4 * Hq * T if T > 0 else 0
+        total += 4 * L + scan_b + ver_b
+        scan += scan_b
+        verify += ver_b
+    return total, scan, verify
+
+
+def cpu_baseline(cfg, x, seqs):
+    """Time the CPU oracle on a bounded sample of sequences of the same workload."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    t0 = time.perf_counter()
+    oracle.step(x["tokens"], x["lens"], x["bank"], None, cfg.n_max, cfg.k, cfg.W, cfg.S,
+                q_bits=x["q"], kc_bits=x["k_ctx"], vc_bits=x["v_ctx"], kt_bits=x["k_tree"],
+                vt_bits=x["v_tree"], seqs=seqs)
+    dt = time.perf_counter() - t0
+    return {"value": len(seqs) / dt, "unit": "drafts/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(seqs)} of {cfg.B} sequences (b={list(seqs)}), full step each, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the batch's sequences are independent and would shard across GPUs with no exchange).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_05742_amd as adapld
+    from paper_2606_05742_amd.synth import BENCH_CONFIG, CONFIGS, make_inputs
+
+    name = args.workload or BENCH_CONFIG
+    cfg = CONFIGS[name]
+    log(f"[bench] generating {name}")
+    x = make_inputs(cfg)
+
+    def up_bf16(a):
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+
+    tokens = torch.from_numpy(x["tokens"]).cuda()
+    lens = torch.from_numpy(x["lens"]).cuda()
+    sets = []
+    for _ in range(2):
+        sets.append(dict(bank=up_bf16(x["bank"]), q=up_bf16(x["q"]), k_ctx=up_bf16(x["k_ctx"]),
+                         v_ctx=up_bf16(x["v_ctx"]), k_tree=up_bf16(x["k_tree"]), v_tree=up_bf16(x["v_tree"])))
+    bufs = adapld.StepBuffers.allocate(cfg.B, cfg.L, cfg.d, cfg.k, cfg.T_max, cfg.Hq, cfg.Hkv, cfg.D)
+    stream = torch.cuda.current_stream()
+
+    def run(i, ev=None):
+        s = sets[i % 2]
+        adapld.lexical_match(tokens, lens, cfg.n_max, cand_pos=bufs.cand_pos, cand_count=bufs.cand_count,
+                             match_n=bufs.match_n)
+        adapld.semantic_topk(s["bank"], lens, bufs.cand_pos, bufs.cand_count, cfg.k, topk_pos=bufs.topk_pos,
+                             topk_score=bufs.topk_score, topk_count=bufs.topk_count, kind=bufs.kind,
+                             ws=bufs.ws_sem)
+        adapld.build_draft_tree(tokens, lens, bufs.topk_pos, bufs.topk_count, bufs.kind, cfg.W, cfg.S,
+                                cfg.T_max, node_token=bufs.node_token, node_parent=bufs.node_parent,
+                                node_depth=bufs.node_depth, node_src=bufs.node_src,
+                                node_count=bufs.node_count, tree_mask=bufs.tree_mask)
+        if ev is not None:
+            ev[0].record(stream)
+        adapld.tree_verify_attn(s["q"], s["k_ctx"], s["v_ctx"], s["k_tree"], s["v_tree"], lens,
+                                bufs.node_count, bufs.tree_mask, out=bufs.out, lse=bufs.lse, ws=bufs.ws_ver)
+        if ev is not None:
+            ev[1].record(stream)
+
+    log(f"[bench] warmup {args.warmup}")
+    for i in range(args.warmup):
+        run(i)
+    torch.cuda.synchronize()
+    cand_count = bufs.cand_count.cpu().numpy()
+    node_count = bufs.node_count.cpu().numpy()
+    kinds = bufs.kind.cpu().numpy()
+
+    log(f"[bench] timing {args.steps} steps")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        run(i, evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    step_ms = t_start.elapsed_time(t_end) / args.steps
+    ver_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    log(f"[bench] step {step_ms * 1e3:.1f} us, verify {ver_ms * 1e3:.1f} us")
+
+    total_b, scan_b, ver_b = algorithmic_bytes(cfg, x["lens"], cand_count, node_count)
+    step_gbs = total_b / (step_ms * 1e-3) / 1e9
+    ver_gbs = ver_b / (ver_ms * 1e-3) / 1e9
+    n_fb = int((cand_count == 0).sum())
+    rec = {
+        "metric": "draft+verify step us and drafts/s per MI355X; achieved HBM GB/s vs peak",
+        "value": cfg.B / (step_ms * 1e-3),
+        "unit": "drafts/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "step_us": step_ms * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": name, "B": cfg.B, "L": cfg.L, "d": cfg.d, "Hq": cfg.Hq, "Hkv": cfg.Hkv,
+                   "D": cfg.D, "n_max": cfg.n_max, "k": cfg.k, "W": cfg.W, "S": cfg.S, "T_max": cfg.T_max},
+        "step_hbm": {"algorithmic_bytes": total_b, "achieved_GBs": step_gbs, "peak_GBs": HBM_PEAK_GBS,
+                     "frac": step_gbs / HBM_PEAK_GBS},
+        "draft_nodes_per_s": float(node_count.sum()) / (step_ms * 1e-3),
+        "fallback_sequences": n_fb,
+        "kinds": {"lex": int((kinds == 1).sum()), "sem": int((kinds == 2).sum()), "none": int((kinds == 0).sum())},
+        "roofline": {"kernel": "tree_verify_attn", "bound": "hbm", "achieved": ver_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": ver_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": ver_b, "launch_us": ver_ms * 1e3},
+    }
+    if not args.no_cpu_baseline:
+        seqs = [b for b in range(min(cfg.B, 4))]
+        log(f"[bench] cpu baseline on sequences {seqs}")
+        rec["cpu_baseline"] = cpu_baseline(cfg, x, seqs)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

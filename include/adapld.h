@@ -1,0 +1,225 @@
+/*
+ * adapld.h -- C ABI of libadapld, the AdaPLD draft-and-verify hot path on
+ * AMD MI355X (gfx950).
+ *
+ * One decoding iteration of AdaPLD (Algorithm 1 of the paper, between two
+ * target-model forward passes) is four calls, enqueued on one HIP stream with
+ * no host synchronisation between them:
+ *
+ *   1. adapld_lexical_match     lexical anchoring (Sec. 3.3)
+ *   2. adapld_semantic_topk     lexical/semantic backoff + hidden-state
+ *                               reranking (Sec. 3.3, Sec. 3.4)
+ *   3. adapld_build_draft_tree  reuse construction as a draft tree
+ *                               (Sec. 3.5, Sec. 3.6)
+ *   4. adapld_tree_verify_attn  tree-masked verify attention (Sec. 3.6)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument is DEVICE memory owned by the caller.  The library
+ *   never allocates, frees or keeps a pointer after a call returns; it holds
+ *   no state between calls and is safe to call from several host threads.
+ * - bf16 tensors are passed as `const uint16_t*` holding the bf16 bit
+ *   patterns.  All tensors are dense, row-major, in the layouts stated below;
+ *   bf16 tensors must be 16-byte aligned.
+ * - `B` sequences are processed per call.  Sequence b has context length
+ *   `lens[b]` (device array), clamped on the device to [0, L_stride];
+ *   `L_stride` is the allocated length per sequence.
+ * - Arguments are validated on the host BEFORE anything is enqueued: on any
+ *   error nothing is launched and the function returns a negative status.
+ *   B == 0 is valid and enqueues nothing.
+ * - Kernels are enqueued on `stream` (0 = the null stream); the call returns
+ *   without waiting.  Faults inside a kernel surface at the caller's next
+ *   synchronisation on that stream.
+ * - Output entries past a per-sequence count are unspecified unless stated.
+ * - Workspace: `ws` is caller-owned device scratch of at least
+ *   adapld_workspace_bytes(op, ...) bytes; its contents need no
+ *   initialisation and are clobbered.  Calls that share one `ws` must not
+ *   overlap in time.
+ */
+#ifndef ADAPLD_H
+#define ADAPLD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every entry point. */
+#define ADAPLD_OK 0
+#define ADAPLD_ERR_NULL_ARG (-1)           /* a required pointer is NULL */
+#define ADAPLD_ERR_INVALID_ARG (-2)        /* a size/shape/alignment is invalid */
+#define ADAPLD_ERR_UNSUPPORTED (-3)        /* valid but outside what the kernels implement */
+#define ADAPLD_ERR_WORKSPACE_TOO_SMALL (-4)
+#define ADAPLD_ERR_HIP (-5)                /* a HIP launch failed; see adapld_last_hip_error */
+
+/* Retrieval outcome of one sequence (the paper's hit-rate categories,
+ * Appendix "Retrieval Hit Rate"). */
+#define ADAPLD_KIND_NONE 0   /* lexical miss and the fallback found nothing: plain AR step */
+#define ADAPLD_KIND_LEX 1    /* lexical hit: candidates reranked */
+#define ADAPLD_KIND_SEM 2    /* lexical miss recovered by the semantic fallback */
+
+/* Operation ids for adapld_workspace_bytes. */
+#define ADAPLD_OP_LEXICAL_MATCH 1
+#define ADAPLD_OP_SEMANTIC_TOPK 2
+#define ADAPLD_OP_BUILD_DRAFT_TREE 3
+#define ADAPLD_OP_TREE_VERIFY_ATTN 4
+
+/* Limits of this implementation (larger values return ADAPLD_ERR_UNSUPPORTED). */
+#define ADAPLD_MAX_NMAX 64
+#define ADAPLD_MAX_K 64
+#define ADAPLD_MAX_HIDDEN 8192
+#define ADAPLD_MAX_TREE_NODES 256
+#define ADAPLD_HEAD_DIM 128
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char* adapld_status_string(int status);
+
+/* The hipError_t of the most recent ADAPLD_ERR_HIP on the calling thread
+ * (0 if none). */
+int adapld_last_hip_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int adapld_version(void);
+
+/* Bytes of device workspace that `op` needs for these sizes (0 if none).
+ * Arguments that an op does not use are ignored.  Returns 0 for invalid
+ * sizes (the entry point itself reports the error). */
+size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_max,
+                              int Hq, int Hkv, int D);
+
+/*
+ * adapld_lexical_match -- lexical anchoring (Sec. 3.3: the exact-match
+ * candidate set of the query anchor, the most recent token), generalised to
+ * the longest matching suffix n-gram.
+ *
+ * For sequence b with context M = tokens[b, 0..L-1], L = lens[b]: for
+ * n = n_max down to 1, C_n = { j in [n-1, L-2] : M[j-n+1..j] == M[L-n..L-1] }.
+ * The first non-empty level n* is kept (n* = 0 and no candidates if none).
+ * n_max = 1 is exactly the paper's single-token match.
+ *
+ *   tokens     int32 [B, L_stride]          token ids
+ *   lens       int32 [B]                    context lengths
+ *   n_max      1..ADAPLD_MAX_NMAX
+ *   cand_pos   int32 [B, L_stride]  (out)   C_{n*} in ascending order
+ *   cand_count int32 [B]            (out)   |C_{n*}|
+ *   match_n    int32 [B]            (out)   n*
+ *
+ * Errors: NULL_ARG for a NULL pointer; INVALID_ARG for B < 0 or
+ * L_stride < 1; UNSUPPORTED for n_max outside 1..ADAPLD_MAX_NMAX.
+ */
+int adapld_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride,
+                         int n_max, int32_t* cand_pos, int32_t* cand_count, int32_t* match_n,
+                         hipStream_t stream);
+
+/*
+ * adapld_semantic_topk -- the lexical/semantic backoff rule (Sec. 3.3) and
+ * hidden-state reranking (Sec. 3.4).
+ *
+ * Score s(r) = cos(bank[b, r], q_b) computed with fp32 accumulation (0 when
+ * either norm is 0), where q_b = query[b] or, if `query` is NULL, the bank
+ * row lens[b]-1.  If cand_count[b] > 0 (lexical hit) the scored rows are
+ * cand_pos[b, 0..cand_count[b]-1] and kind = LEX.  Otherwise (lexical miss)
+ * every row r in [0, L-2] is scored (the semantic fallback), entries with
+ * s < tau are dropped unless tau is NaN (disabled), and kind = SEM if any
+ * entry remains, else NONE.  Rows are ranked by score descending, then
+ * position ascending, and the first min(k, #rows) are returned.  Candidate
+ * positions outside [0, L-1] are skipped.
+ *
+ *   bank       bf16  [B, L_stride, d]       hidden states (row = position)
+ *   query      bf16  [B, d] or NULL
+ *   lens, cand_pos, cand_count              as produced by adapld_lexical_match
+ *   d          8..ADAPLD_MAX_HIDDEN, multiple of 8
+ *   k          1..ADAPLD_MAX_K
+ *   tau        fallback threshold; NaN disables it
+ *   topk_pos   int32 [B, k]       (out)     ranked positions
+ *   topk_score fp32  [B, k]       (out)     their scores
+ *   topk_count int32 [B]          (out)     entries written
+ *   kind       int32 [B]          (out)     ADAPLD_KIND_*
+ *   ws         workspace of adapld_workspace_bytes(ADAPLD_OP_SEMANTIC_TOPK, B, L_stride, d, k, ...)
+ *
+ * Errors: NULL_ARG; INVALID_ARG for bad sizes or misaligned bf16 pointers;
+ * UNSUPPORTED for d or k beyond the limits; WORKSPACE_TOO_SMALL.
+ */
+int adapld_semantic_topk(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
+                         const int32_t* cand_pos, const int32_t* cand_count, int B, int L_stride,
+                         int d, int k, float tau, int32_t* topk_pos, float* topk_score,
+                         int32_t* topk_count, int32_t* kind, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
+
+/*
+ * adapld_build_draft_tree -- reuse construction (Sec. 3.5) organised as a
+ * draft tree (Sec. 3.6).
+ *
+ * Walks the ranked list; the successor token M[r+1] of entry r opens a new
+ * branch unless an earlier branch starts with the same token; at most W
+ * branches.  Each branch is M[r+1 .. min(r+1+S, L-1)]: the branch token and
+ * up to S copied tokens (with a lexical hit, branch 0 is the paper's main
+ * copy path of maximum length S+1).  kind = NONE gives an empty tree.
+ * Nodes are stored branch-major, by depth within a branch:
+ *
+ *   node_token  int32 [B, T_max]  (out)  token id of the node
+ *   node_parent int32 [B, T_max]  (out)  parent node, -1 at depth 0 (the
+ *                                        root is the last context token)
+ *   node_depth  int32 [B, T_max]  (out)  depth; its position is lens[b] + depth
+ *   node_src    int32 [B, T_max]  (out)  memory position the node copies
+ *   node_count  int32 [B]         (out)  T, the number of nodes (<= W*(S+1))
+ *   tree_mask   uint64 [B, T_max, ceil(T_max/64)] (out)  bit v of row u is set
+ *                                        iff v is u or an ancestor of u; every
+ *                                        bit of rows >= T and columns >= T is 0
+ *
+ * Inputs: tokens, lens as above; topk_pos, topk_count, kind from
+ * adapld_semantic_topk with the same k.  Ranked entries outside [0, L-2]
+ * are skipped.
+ *
+ * Errors: NULL_ARG; INVALID_ARG for W < 1, S < 0, k < 1 or
+ * T_max < W*(S+1); UNSUPPORTED for k > ADAPLD_MAX_K or
+ * T_max > ADAPLD_MAX_TREE_NODES.
+ */
+int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const int32_t* topk_pos,
+                            const int32_t* topk_count, const int32_t* kind, int B, int L_stride,
+                            int k, int W, int S, int T_max, int32_t* node_token,
+                            int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
+                            int32_t* node_count, uint64_t* tree_mask, hipStream_t stream);
+
+/*
+ * adapld_tree_verify_attn -- tree attention for verification (Sec. 3.6):
+ * every draft node is scored against the KV cache in one pass.
+ *
+ * For node u < T = node_count[b] and query head h (kv head g = h / (Hq/Hkv)):
+ * the keys are k_ctx[b, g, 0..L-1] followed by k_tree[b, v, g] for every v
+ * with bit v of tree_mask[b, u] set; values likewise.  With logits
+ * z = scale * q . key (fp32 accumulation of bf16 products):
+ *   out[b, u, h] = softmax(z) . values        (bf16)
+ *   lse[b, h, u] = ln sum exp(z)              (fp32)
+ *
+ *   q          bf16 [B, T_max, Hq, D]
+ *   k_ctx      bf16 [B, Hkv, L_stride, D]
+ *   v_ctx      bf16 [B, Hkv, L_stride, D]
+ *   k_tree     bf16 [B, T_max, Hkv, D]
+ *   v_tree     bf16 [B, T_max, Hkv, D]
+ *   lens, node_count, tree_mask             as above
+ *   D          ADAPLD_HEAD_DIM (128)
+ *   out        bf16 [B, T_max, Hq, D]  (out) rows u >= T are not written
+ *   lse        fp32 [B, Hq, T_max]     (out, may be NULL) entries u >= T not written
+ *   ws         workspace of adapld_workspace_bytes(ADAPLD_OP_TREE_VERIFY_ATTN, B, L_stride, 0, 0, T_max, Hq, Hkv, D)
+ *
+ * Errors: NULL_ARG; INVALID_ARG for Hq % Hkv != 0, non-positive sizes,
+ * non-finite scale or misaligned pointers; UNSUPPORTED for D != 128 or
+ * T_max > ADAPLD_MAX_TREE_NODES; WORKSPACE_TOO_SMALL.
+ */
+int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx,
+                            const uint16_t* k_tree, const uint16_t* v_tree, const int32_t* lens,
+                            const int32_t* node_count, const uint64_t* tree_mask, int B,
+                            int L_stride, int T_max, int Hq, int Hkv, int D, float scale,
+                            uint16_t* out, float* lse, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ADAPLD_H */

@@ -5,3 +5,7 @@ behind the C-ABI library ``libadapld.so``; ``binding`` is a thin layer over
 it (argument marshalling only).  A missing library is an error, never a
 fallback.
 """
+from .binding import (  # noqa: F401
+    KIND_LEX, KIND_NONE, KIND_SEM, AdapldError, StepBuffers, build_draft_tree, lexical_match,
+    load_library, semantic_topk, step, tree_verify_attn, workspace_bytes,
+)

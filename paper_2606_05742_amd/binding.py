@@ -1,0 +1,284 @@
+"""ctypes binding of libadapld (argument marshalling only).
+
+Every function takes torch tensors that already live on the GPU, checks their
+dtype, shape, contiguity and device, and passes raw device pointers plus the
+current HIP stream to the C ABI declared in ``include/adapld.h``.  All
+computation happens in the library's HIP kernels; nothing here computes a
+result.  bf16 tensors may be ``torch.bfloat16`` or 16-bit integer views of
+the same bits.  If the library is missing, every call raises AdapldError.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+import torch
+
+KIND_NONE, KIND_LEX, KIND_SEM = 0, 1, 2
+OP_LEXICAL_MATCH, OP_SEMANTIC_TOPK, OP_BUILD_DRAFT_TREE, OP_TREE_VERIFY_ATTN = 1, 2, 3, 4
+HEAD_DIM = 128
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadapld.so")
+
+_c_i32p = ctypes.c_void_p
+_lib = None
+
+
+class AdapldError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(what)
+
+
+# name -> (restype, argtypes) for every function include/adapld.h declares
+SIGNATURES = {
+    "adapld_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "adapld_last_hip_error": (ctypes.c_int, []),
+    "adapld_version": (ctypes.c_int, []),
+    "adapld_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int] * 9),
+    "adapld_lexical_match": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "adapld_semantic_topk": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "adapld_build_draft_tree": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p]),
+    "adapld_tree_verify_attn": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+        ctypes.c_void_p]),
+}
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libadapld.so (once).  Raises AdapldError when it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise AdapldError(-100, f"{path} is missing: build it with `python -m paper_2606_05742_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        lib = load_library()
+        msg = lib.adapld_status_string(status).decode()
+        if status == -5:
+            msg += f" (hipError {lib.adapld_last_hip_error()})"
+        raise AdapldError(status, f"{what}: {msg}")
+
+
+_BF16_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _ptr(t, name, dtypes, shape=None, nullable=False):
+    if t is None:
+        if nullable:
+            return None
+        raise AdapldError(-1, f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise AdapldError(-2, f"{name} must live on the GPU (got {t.device})")
+    if t.dtype not in dtypes:
+        raise AdapldError(-2, f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise AdapldError(-2, f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise AdapldError(-2, f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def workspace_bytes(op, B, L_stride, d=0, k=0, T_max=0, Hq=0, Hkv=0, D=0) -> int:
+    return int(load_library().adapld_workspace_bytes(op, B, L_stride, d, k, T_max, Hq, Hkv, D))
+
+
+def _i32(n, dev):
+    return torch.empty(n, dtype=torch.int32, device=dev)
+
+
+def lexical_match(tokens, lens, n_max, *, cand_pos=None, cand_count=None, match_n=None, stream=None):
+    """Longest-suffix n-gram anchoring; returns (cand_pos, cand_count, match_n)."""
+    lib = load_library()
+    B, L_stride = tokens.shape
+    dev = tokens.device
+    cand_pos = torch.empty((B, L_stride), dtype=torch.int32, device=dev) if cand_pos is None else cand_pos
+    cand_count = _i32(B, dev) if cand_count is None else cand_count
+    match_n = _i32(B, dev) if match_n is None else match_n
+    st = lib.adapld_lexical_match(
+        _ptr(tokens, "tokens", (torch.int32,)), _ptr(lens, "lens", (torch.int32,), (B,)), B, L_stride,
+        n_max, _ptr(cand_pos, "cand_pos", (torch.int32,), (B, L_stride)),
+        _ptr(cand_count, "cand_count", (torch.int32,), (B,)), _ptr(match_n, "match_n", (torch.int32,), (B,)),
+        _stream(stream))
+    _check(st, "adapld_lexical_match")
+    return cand_pos, cand_count, match_n
+
+
+def semantic_topk(bank, lens, cand_pos, cand_count, k, *, tau=None, query=None, topk_pos=None,
+                  topk_score=None, topk_count=None, kind=None, ws=None, stream=None):
+    """Backoff + cosine reranking; returns (topk_pos, topk_score, topk_count, kind)."""
+    lib = load_library()
+    B, L_stride, d = bank.shape
+    dev = bank.device
+    topk_pos = torch.empty((B, k), dtype=torch.int32, device=dev) if topk_pos is None else topk_pos
+    topk_score = torch.empty((B, k), dtype=torch.float32, device=dev) if topk_score is None else topk_score
+    topk_count = _i32(B, dev) if topk_count is None else topk_count
+    kind = _i32(B, dev) if kind is None else kind
+    need = workspace_bytes(OP_SEMANTIC_TOPK, B, L_stride, d, k)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    st = lib.adapld_semantic_topk(
+        _ptr(bank, "bank", _BF16_DTYPES), _ptr(query, "query", _BF16_DTYPES, (B, d), nullable=True),
+        _ptr(lens, "lens", (torch.int32,), (B,)), _ptr(cand_pos, "cand_pos", (torch.int32,), (B, L_stride)),
+        _ptr(cand_count, "cand_count", (torch.int32,), (B,)), B, L_stride, d, k,
+        float("nan") if tau is None else float(tau),
+        _ptr(topk_pos, "topk_pos", (torch.int32,), (B, k)), _ptr(topk_score, "topk_score", (torch.float32,), (B, k)),
+        _ptr(topk_count, "topk_count", (torch.int32,), (B,)), _ptr(kind, "kind", (torch.int32,), (B,)),
+        _ptr(ws, "ws", (torch.uint8,)), ws.numel(), _stream(stream))
+    _check(st, "adapld_semantic_topk")
+    return topk_pos, topk_score, topk_count, kind
+
+
+def build_draft_tree(tokens, lens, topk_pos, topk_count, kind, W, S, T_max=None, *, node_token=None,
+                     node_parent=None, node_depth=None, node_src=None, node_count=None, tree_mask=None,
+                     stream=None):
+    """Draft tree from the ranked list; returns (token, parent, depth, src, count, mask)."""
+    lib = load_library()
+    B, L_stride = tokens.shape
+    k = topk_pos.shape[1]
+    T_max = W * (S + 1) if T_max is None else T_max
+    nw = (T_max + 63) // 64
+    dev = tokens.device
+    mk = lambda t: torch.empty((B, T_max), dtype=torch.int32, device=dev) if t is None else t  # noqa: E731
+    node_token, node_parent, node_depth, node_src = mk(node_token), mk(node_parent), mk(node_depth), mk(node_src)
+    node_count = _i32(B, dev) if node_count is None else node_count
+    tree_mask = torch.empty((B, T_max, nw), dtype=torch.int64, device=dev) if tree_mask is None else tree_mask
+    i32 = (torch.int32,)
+    st = lib.adapld_build_draft_tree(
+        _ptr(tokens, "tokens", i32), _ptr(lens, "lens", i32, (B,)), _ptr(topk_pos, "topk_pos", i32, (B, k)),
+        _ptr(topk_count, "topk_count", i32, (B,)), _ptr(kind, "kind", i32, (B,)), B, L_stride, k, W, S, T_max,
+        _ptr(node_token, "node_token", i32, (B, T_max)), _ptr(node_parent, "node_parent", i32, (B, T_max)),
+        _ptr(node_depth, "node_depth", i32, (B, T_max)), _ptr(node_src, "node_src", i32, (B, T_max)),
+        _ptr(node_count, "node_count", i32, (B,)),
+        _ptr(tree_mask, "tree_mask", (torch.int64, torch.uint64), (B, T_max, nw)), _stream(stream))
+    _check(st, "adapld_build_draft_tree")
+    return node_token, node_parent, node_depth, node_src, node_count, tree_mask
+
+
+def tree_verify_attn(q, k_ctx, v_ctx, k_tree, v_tree, lens, node_count, tree_mask, *, scale=None,
+                     out=None, lse=None, ws=None, with_lse=True, stream=None):
+    """Tree-masked attention of every draft node; returns (out, lse)."""
+    lib = load_library()
+    B, T_max, Hq, D = q.shape
+    Hkv, L_stride = k_ctx.shape[1], k_ctx.shape[2]
+    dev = q.device
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    out = torch.empty((B, T_max, Hq, D), dtype=torch.bfloat16, device=dev) if out is None else out
+    if lse is None and with_lse:
+        lse = torch.empty((B, Hq, T_max), dtype=torch.float32, device=dev)
+    need = workspace_bytes(OP_TREE_VERIFY_ATTN, B, L_stride, 0, 0, T_max, Hq, Hkv, D)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    nw = (T_max + 63) // 64
+    st = lib.adapld_tree_verify_attn(
+        _ptr(q, "q", _BF16_DTYPES), _ptr(k_ctx, "k_ctx", _BF16_DTYPES, (B, Hkv, L_stride, D)),
+        _ptr(v_ctx, "v_ctx", _BF16_DTYPES, (B, Hkv, L_stride, D)),
+        _ptr(k_tree, "k_tree", _BF16_DTYPES, (B, T_max, Hkv, D)),
+        _ptr(v_tree, "v_tree", _BF16_DTYPES, (B, T_max, Hkv, D)),
+        _ptr(lens, "lens", (torch.int32,), (B,)), _ptr(node_count, "node_count", (torch.int32,), (B,)),
+        _ptr(tree_mask, "tree_mask", (torch.int64, torch.uint64), (B, T_max, nw)),
+        B, L_stride, T_max, Hq, Hkv, D, float(scale),
+        _ptr(out, "out", _BF16_DTYPES, (B, T_max, Hq, D)),
+        _ptr(lse, "lse", (torch.float32,), (B, Hq, T_max), nullable=True),
+        _ptr(ws, "ws", (torch.uint8,)), ws.numel(), _stream(stream))
+    _check(st, "adapld_tree_verify_attn")
+    return out, lse
+
+
+@dataclass
+class StepBuffers:
+    """Outputs and workspaces of one step, allocated once and reused."""
+    cand_pos: torch.Tensor
+    cand_count: torch.Tensor
+    match_n: torch.Tensor
+    topk_pos: torch.Tensor
+    topk_score: torch.Tensor
+    topk_count: torch.Tensor
+    kind: torch.Tensor
+    node_token: torch.Tensor
+    node_parent: torch.Tensor
+    node_depth: torch.Tensor
+    node_src: torch.Tensor
+    node_count: torch.Tensor
+    tree_mask: torch.Tensor
+    out: torch.Tensor
+    lse: torch.Tensor
+    ws_sem: torch.Tensor
+    ws_ver: torch.Tensor
+
+    @staticmethod
+    def allocate(B, L_stride, d, k, T_max, Hq, Hkv, D=HEAD_DIM, device="cuda"):
+        i32 = lambda *s: torch.empty(s, dtype=torch.int32, device=device)  # noqa: E731
+        nw = (T_max + 63) // 64
+        ws_sem = torch.empty(max(workspace_bytes(OP_SEMANTIC_TOPK, B, L_stride, d, k), 16),
+                             dtype=torch.uint8, device=device)
+        ws_ver = torch.empty(max(workspace_bytes(OP_TREE_VERIFY_ATTN, B, L_stride, 0, 0, T_max, Hq, Hkv, D), 16),
+                             dtype=torch.uint8, device=device)
+        return StepBuffers(
+            cand_pos=i32(B, L_stride), cand_count=i32(B), match_n=i32(B),
+            topk_pos=i32(B, k), topk_score=torch.empty((B, k), dtype=torch.float32, device=device),
+            topk_count=i32(B), kind=i32(B),
+            node_token=i32(B, T_max), node_parent=i32(B, T_max), node_depth=i32(B, T_max),
+            node_src=i32(B, T_max), node_count=i32(B),
+            tree_mask=torch.empty((B, T_max, nw), dtype=torch.int64, device=device),
+            out=torch.empty((B, T_max, Hq, D), dtype=torch.bfloat16, device=device),
+            lse=torch.empty((B, Hq, T_max), dtype=torch.float32, device=device),
+            ws_sem=ws_sem, ws_ver=ws_ver)
+
+
+def step(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None, query=None,
+         scale=None, buffers: StepBuffers | None = None, stream=None):
+    """One draft-and-verify step: the four entry points back to back on one stream.
+
+    No host synchronisation happens inside; the lexical-hit / fallback decision
+    is taken on the device.  Returns the StepBuffers holding every output.
+    """
+    B, L_stride = tokens.shape
+    T_max = q.shape[1]
+    if buffers is None:
+        buffers = StepBuffers.allocate(B, L_stride, bank.shape[2], k, T_max, q.shape[2], k_ctx.shape[1],
+                                       device=tokens.device)
+    bf = buffers
+    lexical_match(tokens, lens, n_max, cand_pos=bf.cand_pos, cand_count=bf.cand_count, match_n=bf.match_n,
+                  stream=stream)
+    semantic_topk(bank, lens, bf.cand_pos, bf.cand_count, k, tau=tau, query=query, topk_pos=bf.topk_pos,
+                  topk_score=bf.topk_score, topk_count=bf.topk_count, kind=bf.kind, ws=bf.ws_sem, stream=stream)
+    build_draft_tree(tokens, lens, bf.topk_pos, bf.topk_count, bf.kind, W, S, T_max, node_token=bf.node_token,
+                     node_parent=bf.node_parent, node_depth=bf.node_depth, node_src=bf.node_src,
+                     node_count=bf.node_count, tree_mask=bf.tree_mask, stream=stream)
+    tree_verify_attn(q, k_ctx, v_ctx, k_tree, v_tree, lens, bf.node_count, bf.tree_mask, scale=scale,
+                     out=bf.out, lse=bf.lse, ws=bf.ws_ver, stream=stream)
+    return bf

@@ -1,0 +1,142 @@
+// C ABI of libadapld: argument validation, workspace sizing, status reporting.
+// Every check runs on the host before anything is enqueued.
+#include <cmath>
+#include <cstdint>
+
+#include "adapld_internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr int kVersion = 10000;  // 1.0.0
+
+bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return ADAPLD_OK;
+  g_last_hip_error = static_cast<int>(e);
+  return ADAPLD_ERR_HIP;
+}
+
+size_t semantic_ws(int B, int L_stride, int k) {
+  return (size_t)B * adapld::scan_chunks(L_stride) * k * sizeof(uint64_t);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* adapld_status_string(int status) {
+  switch (status) {
+    case ADAPLD_OK: return "ok";
+    case ADAPLD_ERR_NULL_ARG: return "a required pointer argument is NULL";
+    case ADAPLD_ERR_INVALID_ARG: return "invalid size, shape or alignment argument";
+    case ADAPLD_ERR_UNSUPPORTED: return "argument outside the limits this library implements";
+    case ADAPLD_ERR_WORKSPACE_TOO_SMALL: return "workspace smaller than adapld_workspace_bytes()";
+    case ADAPLD_ERR_HIP: return "a HIP launch failed (see adapld_last_hip_error)";
+    default: return "unknown status";
+  }
+}
+
+int adapld_last_hip_error(void) { return g_last_hip_error; }
+
+int adapld_version(void) { return kVersion; }
+
+size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_max, int Hq, int Hkv,
+                              int D) {
+  (void)d;
+  (void)D;
+  if (B <= 0 || L_stride <= 0) return 0;
+  switch (op) {
+    case ADAPLD_OP_SEMANTIC_TOPK:
+      if (k < 1 || k > ADAPLD_MAX_K) return 0;
+      return semantic_ws(B, L_stride, k);
+    case ADAPLD_OP_TREE_VERIFY_ATTN: {
+      if (T_max < 1 || T_max > ADAPLD_MAX_TREE_NODES || Hq < 1 || Hkv < 1 || Hq % Hkv) return 0;
+      const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
+      return adapld::verify_ws_bytes(p, B, Hkv);
+    }
+    default:
+      return 0;
+  }
+}
+
+int adapld_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                         int32_t* cand_pos, int32_t* cand_count, int32_t* match_n,
+                         hipStream_t stream) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!tokens || !lens || !cand_pos || !cand_count || !match_n) return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1) return ADAPLD_ERR_INVALID_ARG;
+  if (n_max < 1 || n_max > ADAPLD_MAX_NMAX) return ADAPLD_ERR_UNSUPPORTED;
+  return hip_status(adapld::launch_lexical_match(tokens, lens, B, L_stride, n_max, cand_pos,
+                                                 cand_count, match_n, stream));
+}
+
+int adapld_semantic_topk(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
+                         const int32_t* cand_pos, const int32_t* cand_count, int B, int L_stride,
+                         int d, int k, float tau, int32_t* topk_pos, float* topk_score,
+                         int32_t* topk_count, int32_t* kind, void* ws, size_t ws_bytes,
+                         hipStream_t stream) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!bank || !lens || !cand_pos || !cand_count || !topk_pos || !topk_score || !topk_count ||
+      !kind || !ws)
+    return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || d < 8 || d % 8 != 0 || k < 1) return ADAPLD_ERR_INVALID_ARG;
+  if (d > ADAPLD_MAX_HIDDEN || k > ADAPLD_MAX_K) return ADAPLD_ERR_UNSUPPORTED;
+  if (misaligned16(bank) || (query && misaligned16(query))) return ADAPLD_ERR_INVALID_ARG;
+  if (ws_bytes < semantic_ws(B, L_stride, k)) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  return hip_status(adapld::launch_semantic_topk(bank, query, lens, cand_pos, cand_count, B,
+                                                 L_stride, d, k, tau, topk_pos, topk_score,
+                                                 topk_count, kind, static_cast<uint64_t*>(ws),
+                                                 stream));
+}
+
+int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const int32_t* topk_pos,
+                            const int32_t* topk_count, const int32_t* kind, int B, int L_stride,
+                            int k, int W, int S, int T_max, int32_t* node_token,
+                            int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
+                            int32_t* node_count, uint64_t* tree_mask, hipStream_t stream) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!tokens || !lens || !topk_pos || !topk_count || !kind || !node_token || !node_parent ||
+      !node_depth || !node_src || !node_count || !tree_mask)
+    return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || k < 1 || W < 1 || S < 0 || T_max < 1) return ADAPLD_ERR_INVALID_ARG;
+  if (k > ADAPLD_MAX_K || T_max > ADAPLD_MAX_TREE_NODES) return ADAPLD_ERR_UNSUPPORTED;
+  if ((long long)W * (S + 1LL) > T_max) return ADAPLD_ERR_INVALID_ARG;
+  return hip_status(adapld::launch_build_draft_tree(tokens, lens, topk_pos, topk_count, kind, B,
+                                                    L_stride, k, W, S, T_max, node_token,
+                                                    node_parent, node_depth, node_src, node_count,
+                                                    tree_mask, stream));
+}
+
+int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx,
+                            const uint16_t* k_tree, const uint16_t* v_tree, const int32_t* lens,
+                            const int32_t* node_count, const uint64_t* tree_mask, int B,
+                            int L_stride, int T_max, int Hq, int Hkv, int D, float scale,
+                            uint16_t* out, float* lse, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!q || !k_ctx || !v_ctx || !k_tree || !v_tree || !lens || !node_count || !tree_mask || !out)
+    return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || T_max < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || !std::isfinite(scale))
+    return ADAPLD_ERR_INVALID_ARG;
+  if (D != ADAPLD_HEAD_DIM || T_max > ADAPLD_MAX_TREE_NODES) return ADAPLD_ERR_UNSUPPORTED;
+  if (misaligned16(q) || misaligned16(k_ctx) || misaligned16(v_ctx) || misaligned16(k_tree) ||
+      misaligned16(v_tree) || misaligned16(out))
+    return ADAPLD_ERR_INVALID_ARG;
+  const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
+  const size_t need = adapld::verify_ws_bytes(p, B, Hkv);
+  if (need > 0 && !ws) return ADAPLD_ERR_NULL_ARG;
+  if (ws_bytes < need) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  if (need > 0 && misaligned16(ws)) return ADAPLD_ERR_INVALID_ARG;
+  return hip_status(adapld::launch_tree_verify_attn(q, k_ctx, v_ctx, k_tree, v_tree, lens,
+                                                    node_count, tree_mask, B, L_stride, T_max, Hq,
+                                                    Hkv, scale, out, lse, ws, p, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,73 @@
+// Internal declarations shared by the kernels and the C-ABI glue of libadapld.
+// Device code targets gfx950 (CDNA4): wave64, MFMA bf16, 160 KiB LDS per CU.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "adapld.h"
+
+namespace adapld {
+
+// ---------------------------------------------------------------- launch plans
+// Host-side shape decisions shared by the workspace query and the launchers,
+// so that both always agree.
+
+// Semantic scan: rows of one sequence are split into chunks of kRowsPerChunk;
+// each chunk is one workgroup of kScanWaves waves that keeps a top-k.
+constexpr int kScanWaves = 4;
+constexpr int kRowsPerChunk = 64;
+
+inline int scan_chunks(int L_stride) {
+  int rows = L_stride > 1 ? L_stride - 1 : 1;
+  // a lexical hit scores at most L_stride candidates; the fallback L_stride-1 rows
+  int r = L_stride > rows ? L_stride : rows;
+  return (r + kRowsPerChunk - 1) / kRowsPerChunk;
+}
+
+// Verify attention: keys are processed in tiles of kKeyTile; query rows
+// (node u, head-in-group) are stacked per kv head, 32 rows per MFMA block.
+constexpr int kKeyTile = 64;
+
+struct VerifyPlan {
+  int G;           // query heads per kv head
+  int rows_max;    // T_max * G stacked query rows per (sequence, kv head)
+  int nb;          // 32-row blocks per wave
+  int waves;       // waves per workgroup
+  int rows_per_wg;
+  int rowgroups;
+  int nsplit;      // context splits
+  int chunk;       // context keys per split (multiple of kKeyTile)
+};
+
+VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv);
+size_t verify_ws_bytes(const VerifyPlan& p, int B, int Hkv);
+
+// ---------------------------------------------------------------- launchers
+// Each returns the hipError_t of its launches (hipSuccess on success).
+hipError_t launch_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride,
+                                int n_max, int32_t* cand_pos, int32_t* cand_count,
+                                int32_t* match_n, hipStream_t stream);
+
+hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
+                                const int32_t* cand_pos, const int32_t* cand_count, int B,
+                                int L_stride, int d, int k, float tau, int32_t* topk_pos,
+                                float* topk_score, int32_t* topk_count, int32_t* kind,
+                                uint64_t* ws_keys, hipStream_t stream);
+
+hipError_t launch_build_draft_tree(const int32_t* tokens, const int32_t* lens,
+                                   const int32_t* topk_pos, const int32_t* topk_count,
+                                   const int32_t* kind, int B, int L_stride, int k, int W, int S,
+                                   int T_max, int32_t* node_token, int32_t* node_parent,
+                                   int32_t* node_depth, int32_t* node_src, int32_t* node_count,
+                                   uint64_t* tree_mask, hipStream_t stream);
+
+hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx,
+                                   const uint16_t* k_tree, const uint16_t* v_tree,
+                                   const int32_t* lens, const int32_t* node_count,
+                                   const uint64_t* tree_mask, int B, int L_stride, int T_max,
+                                   int Hq, int Hkv, float scale, uint16_t* out, float* lse,
+                                   void* ws, const VerifyPlan& plan, hipStream_t stream);
+
+}  // namespace adapld

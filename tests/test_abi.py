@@ -1,0 +1,120 @@
+"""The C-ABI library loads, exports every declared symbol and validates
+arguments on the host (no compute call is made: every call below carries an
+invalid argument, which the library rejects before enqueueing anything)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_2606_05742_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "adapld.h")
+OK, NULL, INVALID, UNSUPPORTED, WS_SMALL = 0, -1, -2, -3, -4
+P = ctypes.c_void_p(0x10000)  # never dereferenced: validation fails first
+N = None
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return binding.load_library()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(adapld_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) == 8
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in binding.SIGNATURES, n
+
+
+def test_status_strings(lib):
+    for code in (OK, NULL, INVALID, UNSUPPORTED, WS_SMALL, -5, 123):
+        assert lib.adapld_status_string(code)
+    assert lib.adapld_version() == 10000
+    assert lib.adapld_last_hip_error() == 0
+
+
+def test_workspace_sizes(lib):
+    ws = lib.adapld_workspace_bytes
+    assert ws(1, 16, 8192, 4096, 8, 52, 32, 8, 128) == 0          # lexical needs none
+    sem = ws(2, 16, 8192, 4096, 8, 0, 0, 0, 0)
+    assert sem == 16 * math.ceil(8192 / 64) * 8 * 8
+    assert ws(2, 16, 8192, 4096, 65, 0, 0, 0, 0) == 0              # k beyond the limit
+    assert ws(4, 16, 8192, 0, 0, 52, 32, 8, 128) > 0
+    assert ws(4, 16, 8192, 0, 0, 52, 32, 7, 128) == 0              # Hq % Hkv != 0
+    assert ws(9, 16, 8192, 0, 0, 52, 32, 8, 128) == 0
+
+
+def test_lexical_validation(lib):
+    f = lib.adapld_lexical_match
+    assert f(N, N, 0, 0, 0, N, N, N, N) == OK                      # B = 0: nothing to do
+    assert f(N, P, 2, 16, 3, P, P, P, N) == NULL
+    assert f(P, P, -1, 16, 3, P, P, P, N) == INVALID
+    assert f(P, P, 2, 0, 3, P, P, P, N) == INVALID
+    assert f(P, P, 2, 16, 0, P, P, P, N) == UNSUPPORTED
+    assert f(P, P, 2, 16, 65, P, P, P, N) == UNSUPPORTED
+
+
+def test_semantic_validation(lib):
+    f = lib.adapld_semantic_topk
+    nan = float("nan")
+    args = lambda **kw: [kw.get(n, v) for n, v in [  # noqa: E731
+        ("bank", P), ("query", N), ("lens", P), ("cand_pos", P), ("cand_count", P), ("B", 2), ("L", 64),
+        ("d", 256), ("k", 8), ("tau", nan), ("tp", P), ("ts", P), ("tc", P), ("kind", P), ("ws", P),
+        ("wsb", 1 << 20), ("st", N)]]
+    assert f(*args(bank=N)) == NULL
+    assert f(*args(ws=N)) == NULL
+    assert f(*args(d=12)) == INVALID
+    assert f(*args(d=0)) == INVALID
+    assert f(*args(k=0)) == INVALID
+    assert f(*args(k=65)) == UNSUPPORTED
+    assert f(*args(d=8200)) == UNSUPPORTED
+    assert f(*args(bank=ctypes.c_void_p(0x10008))) == INVALID      # misaligned bf16 rows
+    assert f(*args(wsb=16)) == WS_SMALL
+
+
+def test_tree_validation(lib):
+    f = lib.adapld_build_draft_tree
+    args = lambda **kw: [kw.get(n, v) for n, v in [  # noqa: E731
+        ("tok", P), ("lens", P), ("tp", P), ("tc", P), ("kind", P), ("B", 2), ("L", 64), ("k", 8),
+        ("W", 4), ("S", 5), ("T", 24), ("nt", P), ("np", P), ("nd", P), ("ns", P), ("nc", P),
+        ("mask", P), ("st", N)]]
+    assert f(*args(mask=N)) == NULL
+    assert f(*args(W=0)) == INVALID
+    assert f(*args(S=-1)) == INVALID
+    assert f(*args(T=23)) == INVALID                               # T_max < W(S+1)
+    assert f(*args(k=65)) == UNSUPPORTED
+    assert f(*args(T=257, W=1, S=0)) == UNSUPPORTED
+
+
+def test_verify_validation(lib):
+    f = lib.adapld_tree_verify_attn
+    args = lambda **kw: [kw.get(n, v) for n, v in [  # noqa: E731
+        ("q", P), ("kc", P), ("vc", P), ("kt", P), ("vt", P), ("lens", P), ("nc", P), ("mask", P),
+        ("B", 2), ("L", 64), ("T", 24), ("Hq", 8), ("Hkv", 2), ("D", 128), ("scale", 0.1), ("out", P),
+        ("lse", N), ("ws", P), ("wsb", 1 << 30), ("st", N)]]
+    assert f(*args(out=N)) == NULL
+    assert f(*args(Hkv=3)) == INVALID
+    assert f(*args(D=64)) == UNSUPPORTED
+    assert f(*args(T=300)) == UNSUPPORTED
+    assert f(*args(scale=float("inf"))) == INVALID
+    assert f(*args(q=ctypes.c_void_p(0x10002))) == INVALID
+    # L = 8192 splits the context, so a workspace is required
+    assert lib.adapld_workspace_bytes(4, 2, 8192, 0, 0, 24, 8, 2, 128) > 0
+    assert f(*args(L=8192, wsb=0)) == WS_SMALL
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    t = torch.zeros((2, 8), dtype=torch.int32)
+    with pytest.raises(binding.AdapldError):
+        binding.lexical_match(t, torch.zeros(2, dtype=torch.int32), 2)

@@ -1,0 +1,211 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Small seeded cases compare every output of every sequence; the five
+full-size workloads run in the launch configuration the benchmark times and
+compare every lexical, ranking and tree output plus sampled verify rows.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_05742_amd as adapld
+from paper_2606_05742_amd.synth import CONFIGS, f32_to_bf16_bits, make_inputs, small_config
+from parity_helpers import (LazyBank, bf16_to_np_bits, chain_subproblem, check_ranked, check_tree,
+                            check_verify, dev_bf16, dev_i32)
+
+pytestmark = pytest.mark.gpu
+
+
+def log(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+def upload(x):
+    return dict(tokens=dev_i32(x["tokens"]), lens=dev_i32(x["lens"]), bank=dev_bf16(x["bank"]),
+                q=dev_bf16(x["q"]), k_ctx=dev_bf16(x["k_ctx"]), v_ctx=dev_bf16(x["v_ctx"]),
+                k_tree=dev_bf16(x["k_tree"]), v_tree=dev_bf16(x["v_tree"]))
+
+
+def run_step(cfg, d, tau=None, query=None):
+    bf = adapld.step(d["tokens"], d["lens"], d["bank"], d["q"], d["k_ctx"], d["v_ctx"], d["k_tree"],
+                     d["v_tree"], n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, tau=tau, query=query)
+    torch.cuda.synchronize()
+    g = {}
+    for name in ("cand_pos", "cand_count", "match_n", "topk_pos", "topk_score", "topk_count", "kind",
+                 "node_token", "node_parent", "node_depth", "node_src", "node_count", "tree_mask", "lse"):
+        g[name] = getattr(bf, name).cpu().numpy()
+    g["out"] = bf.out.float().cpu().numpy()
+    return g
+
+
+def check_all(cfg, x, g, tau=None, query_bits=None, verify_nodes=None, seqs=None, ctx=""):
+    """Compare the GPU step with the oracle; verify_nodes=None checks every node."""
+    B = x["tokens"].shape[0]
+    seqs = range(B) if seqs is None else seqs
+    kinds = []
+    for b in seqs:
+        c = f"{ctx} b={b}"
+        L = int(x["lens"][b])
+        M = x["tokens"][b, :L]
+        n, C = oracle.lexical_match(M, cfg.n_max)
+        assert int(g["match_n"][b]) == n, f"{c}: n* {int(g['match_n'][b])} != {n}"
+        cnt = int(g["cand_count"][b])
+        assert cnt == len(C), f"{c}: |C| {cnt} != {len(C)}"
+        np.testing.assert_array_equal(g["cand_pos"][b, :cnt], C, err_msg=c)
+        bank = LazyBank(x["bank"][b], L)
+        qv = None if query_bits is None else oracle.bf16_bits_to_f64(query_bits[b])
+        kind = int(g["kind"][b])
+        tc = int(g["topk_count"][b])
+        gpos = [int(p) for p in g["topk_pos"][b, :tc]]
+        check_ranked(bank, qv, C, cfg.k, tau, kind, gpos, [float(s) for s in g["topk_score"][b, :tc]], c)
+        kinds.append(kind)
+        t = check_tree(M, kind, gpos, cfg.W, cfg.S, g, b, c)
+        T = t["T"]
+        if T == 0:
+            continue
+        nodes = range(T) if verify_nodes is None else sorted(set(min(u, T - 1) for u in verify_nodes))
+        scale = 1.0 / math.sqrt(cfg.D)
+        Kc = oracle.bf16_bits_to_f64(x["k_ctx"][b, :, :L])
+        Vc = oracle.bf16_bits_to_f64(x["v_ctx"][b, :, :L])
+        if verify_nodes is None:
+            O, LSE = oracle.tree_verify_attn(
+                oracle.bf16_bits_to_f64(x["q"][b, :T]), Kc, Vc, oracle.bf16_bits_to_f64(x["k_tree"][b, :T]),
+                oracle.bf16_bits_to_f64(x["v_tree"][b, :T]), t["mask"], L, scale)
+            check_verify(g["out"][b, :T], g["lse"][b, :, :T], O, LSE, c)
+        else:
+            for u in nodes:
+                path, cm = chain_subproblem(t["parent"], u)
+                O, LSE = oracle.tree_verify_attn(
+                    oracle.bf16_bits_to_f64(x["q"][b, path]), Kc, Vc,
+                    oracle.bf16_bits_to_f64(x["k_tree"][b, path]), oracle.bf16_bits_to_f64(x["v_tree"][b, path]),
+                    cm, L, scale)
+                check_verify(g["out"][b, u], g["lse"][b, :, u], O[-1], LSE[:, -1], f"{c} u={u}")
+    return kinds
+
+
+SMALL = [
+    dict(),                                                         # GQA 8/2, d=256
+    dict(B=4, L=700, d=512, Hq=4, Hkv=4, k=8, W=4, S=7, n_max=4, seed=21, forced_every=2),
+    dict(B=2, L=1500, d=1040, Hq=12, Hkv=3, k=16, W=8, S=3, n_max=2, seed=22, V=30),
+    dict(B=5, L=130, d=64, Hq=16, Hkv=2, k=64, W=16, S=1, n_max=5, seed=23, V=8),
+    dict(B=3, L=2100, d=4096, Hq=32, Hkv=8, k=8, W=4, S=12, n_max=4, seed=24, forced_every=3),
+]
+
+
+@pytest.mark.parametrize("kw", SMALL, ids=[f"small{i}" for i in range(len(SMALL))])
+def test_step_small(kw):
+    cfg = small_config(**kw)
+    x = make_inputs(cfg)
+    g = run_step(cfg, upload(x))
+    kinds = check_all(cfg, x, g, ctx=str(kw))
+    log("kinds", kinds)
+
+
+def test_step_ragged_lengths():
+    cfg = small_config(B=8, L=600, d=256, Hq=8, Hkv=2, k=8, W=4, S=6, n_max=3, seed=31)
+    lens = [600, 1, 0, 2, 3, 4, 577, 65]
+    x = make_inputs(cfg, lens=lens)
+    g = run_step(cfg, upload(x))
+    check_all(cfg, x, g, ctx="ragged")
+    assert int(g["node_count"][1]) == 0 and int(g["node_count"][2]) == 0
+    assert int(g["kind"][2]) == adapld.KIND_NONE
+
+
+def test_all_equal_tokens_and_duplicate_rows():
+    cfg = small_config(B=2, L=200, d=128, Hq=4, Hkv=1, k=12, W=3, S=4, n_max=4, seed=41)
+    x = make_inputs(cfg)
+    x["tokens"][0, :] = 7                         # every window matches
+    x["bank"][1, 50:120] = x["bank"][1, 10]       # exact duplicate rows tie exactly
+    x["tokens"][1, -1] = 10 ** 6                  # forced lexical miss
+    x["bank"][1, -1] = x["bank"][1, 10]
+    g = run_step(cfg, upload(x))
+    check_all(cfg, x, g, ctx="dups")
+    assert list(g["topk_pos"][1, :12]) == [10] + list(range(50, 61))
+
+
+@pytest.mark.parametrize("tau", [0.1, 1.5, -2.0])
+def test_tau(tau):
+    cfg = small_config(B=6, L=400, d=256, Hq=8, Hkv=2, k=8, W=4, S=5, n_max=3, seed=51, forced_every=2)
+    x = make_inputs(cfg)
+    g = run_step(cfg, upload(x), tau=tau)
+    kinds = check_all(cfg, x, g, tau=tau, ctx=f"tau={tau}")
+    if tau > 1:
+        assert all(k_ in (adapld.KIND_LEX, adapld.KIND_NONE) for k_ in kinds)
+        assert adapld.KIND_NONE in kinds
+
+
+def test_explicit_query():
+    cfg = small_config(B=3, L=300, d=256, Hq=8, Hkv=2, k=6, W=3, S=5, seed=61, forced_every=1)
+    x = make_inputs(cfg)
+    rng = np.random.default_rng(0)
+    qbits = x["bank"][np.arange(3), rng.integers(0, 299, size=3)].copy()
+    g = run_step(cfg, upload(x), query=dev_bf16(qbits))
+    check_all(cfg, x, g, query_bits=qbits, ctx="query")
+
+
+def test_verify_mask_leak_and_peaked():
+    """Non-ancestor tree keys aligned with a node's query must not move its output;
+    a sharpened softmax (Q x 4) keeps the relative error small."""
+    cfg = small_config(B=2, L=900, d=128, Hq=8, Hkv=2, k=8, W=4, S=6, seed=71)
+    x = make_inputs(cfg)
+    d = upload(x)
+    g0 = run_step(cfg, d)
+    for b in range(2):
+        T = int(g0["node_count"][b])
+        u = T - 1
+        mask_u = g0["tree_mask"][b, u].view(np.uint64)
+        others = [v for v in range(T) if not (int(mask_u[v // 64]) >> (v % 64)) & 1]
+        assert others, "tree has a single branch"
+        kt = x["k_tree"].copy()
+        for v in others:
+            for h in range(cfg.Hkv):
+                q32 = oracle.bf16_bits_to_f64(x["q"][b, u, h * cfg.G]).astype(np.float32)
+                kt[b, v, h] = f32_to_bf16_bits(30.0 * q32)
+        g1 = run_step(cfg, dict(d, k_tree=dev_bf16(kt)))
+        np.testing.assert_array_equal(g1["out"][b, u], g0["out"][b, u])
+        assert not np.array_equal(g1["out"][b, others[0]], g0["out"][b, others[0]])
+    xq = dict(x)
+    xq["q"] = f32_to_bf16_bits(oracle.bf16_bits_to_f64(x["q"]).astype(np.float32) * 4.0)
+    g2 = run_step(cfg, dict(d, q=dev_bf16(xq["q"])))
+    check_all(cfg, xq, g2, ctx="peaked")
+
+
+def test_deterministic_repeats():
+    cfg = small_config(B=4, L=3000, d=512, Hq=16, Hkv=4, k=16, W=6, S=6, n_max=3, seed=81, forced_every=2)
+    x = make_inputs(cfg)
+    d = upload(x)
+    ref = run_step(cfg, d)
+    for _ in range(5):
+        g = run_step(cfg, d)
+        for key in ref:
+            np.testing.assert_array_equal(g[key], ref[key], err_msg=key)
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_full_config(name):
+    cfg = CONFIGS[name]
+    log(f"[{name}] generating")
+    x = make_inputs(cfg)
+    log(f"[{name}] uploading and running")
+    g = run_step(cfg, upload(x))
+    log(f"[{name}] comparing")
+    nodes = [0, cfg.S, cfg.T_max - 1]
+    seqs = sorted(set([0, cfg.B - 1] + [b for b in range(cfg.B) if x["forced"][b]][:2]))
+    # lexical and ranking on every sequence, verify on sampled sequences and nodes
+    kinds = check_all(cfg, x, g, verify_nodes=nodes, seqs=seqs, ctx=name)
+    rest = [b for b in range(cfg.B) if b not in seqs]
+    for b in rest:
+        L = int(x["lens"][b])
+        n, C = oracle.lexical_match(x["tokens"][b, :L], cfg.n_max)
+        assert int(g["match_n"][b]) == n and int(g["cand_count"][b]) == len(C)
+        np.testing.assert_array_equal(g["cand_pos"][b, :len(C)], C)
+        tc = int(g["topk_count"][b])
+        gpos = [int(p) for p in g["topk_pos"][b, :tc]]
+        check_ranked(LazyBank(x["bank"][b], L), None, C, cfg.k, None, int(g["kind"][b]), gpos,
+                     [float(s) for s in g["topk_score"][b, :tc]], f"{name} b={b}")
+        check_tree(x["tokens"][b, :L], int(g["kind"][b]), gpos, cfg.W, cfg.S, g, b, f"{name} b={b}")
+    log(f"[{name}] kinds(sampled)={kinds} fallback={int((g['cand_count'] == 0).sum())}/{cfg.B}")
