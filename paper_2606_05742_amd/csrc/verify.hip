@@ -1,20 +1,29 @@
-// Tree-masked verify attention (Sec. 3.6: all draft paths scored in one
+// Tree-masked verify attention (Sec. 3.6: all draft paths are scored in one
 // target forward with tree attention).
 //
-// Work decomposition.  For one sequence b and kv head g, the T*G query rows
-// (node u, query head g*G + i) are stacked row = u*G + i, so the G heads that
-// share a kv head share every K/V byte read.  A workgroup owns up to
-// waves*NB*32 stacked rows and one split of the context keys; the last split
-// also takes the tree keys.  Grid = (splits, row groups, B*Hkv).
+// Work decomposition.  For one sequence b and kv head g the T*G query rows
+// (node u, query head g*G + i) are stacked as row = u*G + i, so the G heads
+// that share a kv head share every K/V byte read from HBM.  A workgroup of 4
+// waves (one per SIMD) owns 4*NB*32 stacked rows and one split of the context
+// keys; the last split also takes the tree keys.  Grid = (splits, row groups,
+// B*Hkv).
 //
-// Per 64-key tile the workgroup stages K (row-major) and V (transposed to
-// [dim][key]) in LDS; each wave then computes S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16 (A = K rows from LDS, B = the wave's Q block held
-// in registers), so every lane owns one query column and 16 keys of it:
-// softmax bookkeeping (running max, rescale) is lane-local except one swap
-// with the lane 32 away.  P^T is fed straight back as the B operand of
-// O^T = V^T P^T; the MFMA's k index is permuted consistently on both operands
-// so no shuffle is needed.  Logits are fp32 in the log2 domain.
+// Memory pipeline.  K and V tiles of 64 keys stream through a 3-stage LDS ring
+// with direct-to-LDS loads (global_load_lds_dwordx4): no VGPR staging, and two
+// tiles are in flight while the third is consumed.  Each 256-byte key row is
+// stored with its 16-byte chunks XOR-swizzled by the row index, which keeps
+// both LDS read patterns below free of bank conflicts.
+//
+// Math.  S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (A = K rows read from LDS,
+// B = the wave's query block held in registers) leaves every lane owning one
+// query column and 16 keys of it, so the online softmax is lane-local except
+// for one v_permlane32_swap.  P^T goes straight back as the B operand of
+// O^T = V^T P^T; the A operand V^T is read with ds_read_b64_tr_b16, which
+// transposes 16-bit elements across lanes on the fly, so V stays row-major in
+// LDS.  The MFMA k index of P and V is permuted identically, so no shuffle is
+// needed.  Logits are fp32 in the log2 domain; the running max is only moved
+// when it grows by more than 8 (a factor 256), which keeps the rescale of the
+// output accumulators off the common path.
 //
 // Splits write unnormalised partial outputs with their running max and sum to
 // the workspace; a combine kernel merges them with log-sum-exp weights.
@@ -27,15 +36,27 @@ namespace adapld {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
-constexpr int kD = ADAPLD_HEAD_DIM;
-constexpr int kKsStride = kD + 8;         // bf16 per K row in LDS (pad against bank conflicts)
-constexpr int kVsStride = kKeyTile + 4;   // bf16 per V^T row in LDS
-constexpr int kMaxWaves = 8;
+constexpr int kD = ADAPLD_HEAD_DIM;           // 128 bf16 = 256 bytes per key row
+constexpr int kRowBytes = kD * 2;
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * kWave;
+constexpr int kStages = 3;
+constexpr int kTileBytes = kKeyTile * kRowBytes;  // 16 KiB for K (and for V)
+constexpr int kLoadsPerWave = 2 * kTileBytes / 1024 / kWaves;  // 1 KiB per wave-wide load
 constexpr int kMaskWords = (ADAPLD_MAX_TREE_NODES + 63) / 64;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kRescaleSlack = 8.0f;         // log2 units the running max may lag
+
+static_assert(kLoadsPerWave == 8, "the vmcnt values in wait_tile_and_sync assume 8 loads per wave per tile");
 
 struct VerifyArgs {
   const uint16_t* q;
@@ -56,15 +77,63 @@ struct VerifyArgs {
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// NB = 2 needs more than 256 VGPRs, so it runs one wave per SIMD (4 waves).
+// Physical 16-byte chunk of logical chunk c in key row r is c ^ swz(r).
+__device__ __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
+
+// s_waitcnt vmcnt(n) (gfx9 encoding, n < 64); lgkmcnt and expcnt unconstrained.
+template <int N>
+__device__ __forceinline__ void waitcnt_vm() {
+  __builtin_amdgcn_s_waitcnt(0x0f70 | (N & 15) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
+
+// One wave-wide direct-to-LDS load: lane i's 16 bytes at gptr land at
+// lds_base + 16*i.  Written as inline asm so that the compiler does not treat
+// every later LDS read as possibly aliasing the in-flight load (it would wait
+// for all outstanding loads there); the pipeline below waits explicitly.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+
+// Issue this wave's share of one K/V tile: rows [16*wave, 16*wave + 16) of K and
+// of V, four rows (1 KiB) per instruction.  Keys past kend re-read key kend-1
+// (in bounds); their logits are masked.
+__device__ __forceinline__ void issue_tile(const uint16_t* kb, const uint16_t* vb, size_t stride,
+                                           int k0, int kend, uint32_t lk, uint32_t lv, int wave,
+                                           int lane) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row0 = 16 * wave + 4 * i;
+    const int row = row0 + (lane >> 4);
+    const int c = (lane & 15) ^ swz(row);
+    const size_t key = (size_t)min(k0 + row, kend - 1);
+    const uint32_t off = __builtin_amdgcn_readfirstlane(row0 * kRowBytes);
+    dma16(kb + key * stride + c * 8, lk + off);
+    dma16(vb + key * stride + c * 8, lv + off);
+  }
+}
+
+// Wait for this wave's loads of the current tile, then for every wave's (the
+// barrier).  The asm memory clobber keeps LDS reads from moving above it.
+__device__ __forceinline__ void wait_tile_and_sync(int later) {
+  if (later >= 2) asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
+  else if (later == 1) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 template <int NB>
-__global__ __launch_bounds__((NB == 1 ? kMaxWaves : 4) * kWave) void tree_verify_kernel(const VerifyArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeyTile * kKsStride];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[kD * kVsStride];
+__global__ __launch_bounds__(kThreads, 1) void tree_verify_kernel(const VerifyArgs a) {
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * 2 * kTileBytes];
+  __shared__ uint64_t s_mask[ADAPLD_MAX_TREE_NODES * kMaskWords];
 
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int nthreads = blockDim.x;
   const int split = blockIdx.x;
   const int bg = blockIdx.z;
   const int b = bg / a.Hkv;
@@ -73,8 +142,7 @@ __global__ __launch_bounds__((NB == 1 ? kMaxWaves : 4) * kWave) void tree_verify
   const int L = min(max(a.lens[b], 0), a.L_stride);
   const int G = a.G;
   const int rows = T * G;
-  const int rows_per_wg = (nthreads / kWave) * NB * 32;
-  const int row_base = blockIdx.y * rows_per_wg;
+  const int row_base = blockIdx.y * (kWaves * NB * 32);
   if (row_base >= rows) return;
 
   const int c0 = split * a.chunk;
@@ -85,7 +153,6 @@ __global__ __launch_bounds__((NB == 1 ? kMaxWaves : 4) * kWave) void tree_verify
 
   // Query fragments (B operand): lane holds dims [16*ds + 8*half, +8) of its row.
   bf16x8_t qf[NB][kD / 16];
-  uint64_t mk[NB][kMaskWords];
   int qrow[NB], qu[NB], qh[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -100,10 +167,11 @@ __global__ __launch_bounds__((NB == 1 ? kMaxWaves : 4) * kWave) void tree_verify
 #pragma unroll
     for (int ds = 0; ds < kD / 16; ++ds)
       qf[nb][ds] = as_bf16x8(valid ? *reinterpret_cast<const uint4*>(qp + 16 * ds) : make_uint4(0, 0, 0, 0));
-#pragma unroll
-    for (int w = 0; w < kMaskWords; ++w)
-      mk[nb][w] = (valid && w < a.nw) ? a.tree_mask[((size_t)b * a.T_max + u) * a.nw + w] : 0ull;
   }
+  if (do_tree)
+    for (int i = threadIdx.x; i < T * a.nw; i += kThreads) s_mask[i] = a.tree_mask[(size_t)b * a.T_max * a.nw + i];
+  waitcnt_vm<0>();   // the query loads retire here, on every path, before the pipeline starts
+  __syncthreads();   // mask table visible
 
   float m_run[NB], l_run[NB];
   f32x16_t o[NB][kD / 32];
@@ -115,116 +183,140 @@ __global__ __launch_bounds__((NB == 1 ? kMaxWaves : 4) * kWave) void tree_verify
     for (int db = 0; db < kD / 32; ++db) o[nb][db] = f32x16_t{};
   }
 
-  const int n_ctx_tiles = c1 > c0 ? (c1 - c0 + kKeyTile - 1) / kKeyTile : 0;
-  const int n_tree_tiles = do_tree ? (T + kKeyTile - 1) / kKeyTile : 0;
-  const size_t ctx_base = (size_t)bg * a.L_stride * kD;
-  const size_t tree_base = ((size_t)b * a.T_max * a.Hkv + g) * kD;
+  const int n_ctx = c1 > c0 ? (c1 - c0 + kKeyTile - 1) / kKeyTile : 0;
+  const int n_tiles = n_ctx + (do_tree ? (T + kKeyTile - 1) / kKeyTile : 0);
+  const uint16_t* kc = a.k_ctx + (size_t)bg * a.L_stride * kD;
+  const uint16_t* vc = a.v_ctx + (size_t)bg * a.L_stride * kD;
+  const size_t tree_off = ((size_t)b * a.T_max * a.Hkv + g) * kD;
   const size_t tree_stride = (size_t)a.Hkv * kD;
 
-  for (int t = 0; t < n_ctx_tiles + n_tree_tiles; ++t) {
-    const bool is_tree = t >= n_ctx_tiles;
-    const int k0 = is_tree ? (t - n_ctx_tiles) * kKeyTile : c0 + t * kKeyTile;
+  const uint32_t smem_base = lds_addr(smem);
+  auto issue = [&](int t) {
+    const uint32_t lk = smem_base + (t % kStages) * 2 * kTileBytes;
+    if (t < n_ctx)
+      issue_tile(kc, vc, kD, c0 + t * kKeyTile, c1, lk, lk + kTileBytes, wave, lane);
+    else
+      issue_tile(a.k_tree + tree_off, a.v_tree + tree_off, tree_stride, (t - n_ctx) * kKeyTile, T, lk,
+                 lk + kTileBytes, wave, lane);
+  };
+
+#pragma unroll
+  for (int t = 0; t < kStages - 1; ++t)
+    if (t < n_tiles) issue(t);
+
+  const float sl2 = a.scale_log2;
+  // Lane-dependent LDS byte offsets within a stage.  K fragment for dims
+  // [16*ds + 8*half, +8) of key row kb*32 + col: kofs[ds] + kb*32*kRowBytes.
+  // Transposed V reads: each 16-lane group covers 4 keys x 16 dims; the key
+  // rows are kb*32 + 16*s2 + vkey (+8), whose swizzle depends on vkey only.
+  int kofs[kD / 16];
+#pragma unroll
+  for (int ds = 0; ds < kD / 16; ++ds) kofs[ds] = col * kRowBytes + (((2 * ds + half) ^ swz(col)) << 4);
+  const int vkey = 4 * half + ((lane & 15) >> 2);
+  const int vdim = (lane & 16) + 4 * (lane & 3);
+  int vofs[2][kD / 32];
+#pragma unroll
+  for (int db = 0; db < kD / 32; ++db) {
+    const int cch = (db * 32 + vdim) >> 3;
+    vofs[0][db] = vkey * kRowBytes + ((cch ^ swz(vkey)) << 4) + (vdim & 7) * 2;
+    vofs[1][db] = (vkey + 8) * kRowBytes + ((cch ^ swz(vkey + 8)) << 4) + (vdim & 7) * 2;
+  }
+  for (int t = 0; t < n_tiles; ++t) {
+    if (t + kStages - 1 < n_tiles) issue(t + kStages - 1);
+    wait_tile_and_sync(min(kStages - 1, n_tiles - 1 - t));
+    const uint8_t* lk = smem + (t % kStages) * 2 * kTileBytes;
+    const uint8_t* lv = lk + kTileBytes;
+    const bool is_tree = t >= n_ctx;
+    const int k0 = is_tree ? (t - n_ctx) * kKeyTile : c0 + t * kKeyTile;
     const int kend = is_tree ? T : c1;
-    const uint16_t* kb = is_tree ? a.k_tree + tree_base : a.k_ctx + ctx_base;
-    const uint16_t* vb = is_tree ? a.v_tree + tree_base : a.v_ctx + ctx_base;
-    const size_t kstride = is_tree ? tree_stride : (size_t)kD;
+    const bool need_mask = is_tree || k0 + kKeyTile > kend;
+    uint64_t mword[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      mword[nb] = (is_tree && qrow[nb] < rows) ? s_mask[qu[nb] * a.nw + (k0 >> 6)] : 0ull;
 
-    // Stage the tile: 16 chunks of 8 dims per key; 16 consecutive threads read one 256-byte row.
-    for (int c = threadIdx.x; c < kKeyTile * (kD / 8); c += nthreads) {
-      const int kr = c >> 4;
-      const int d0 = (c & 15) * 8;
-      const int key = k0 + kr;
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-      if (key < kend) {
-        kv = *reinterpret_cast<const uint4*>(kb + key * kstride + d0);
-        vv = *reinterpret_cast<const uint4*>(vb + key * kstride + d0);
-      }
-      *reinterpret_cast<uint4*>(&Ks[kr * kKsStride + d0]) = kv;
-      const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll 1   // unrolling lets the scheduler overlap the halves and spill
+    for (int kb = 0; kb < 2; ++kb) {
+      // S^T for 32 keys; each K fragment feeds NB query blocks.
+      f32x16_t s[NB];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        Vs[(d0 + 2 * i) * kVsStride + kr] = (uint16_t)(w[i] & 0xffffu);
-        Vs[(d0 + 2 * i + 1) * kVsStride + kr] = (uint16_t)(w[i] >> 16);
+      for (int nb = 0; nb < NB; ++nb) s[nb] = f32x16_t{};
+      const uint8_t* kbase = lk + kb * 32 * kRowBytes;
+#pragma unroll
+      for (int ds = 0; ds < kD / 16; ++ds) {
+        const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(kbase + kofs[ds]);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[nb][ds], s[nb], 0, 0, 0);
       }
-    }
-    __syncthreads();
 
+      // Online softmax; P packed to bf16 in MFMA B-operand order.
+      bf16x8_t pb[NB][2];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      // S^T block per 32 keys: lane holds keys 8*(r/4) + 4*half + r%4 of its query column.
-      f32x16_t s[kKeyTile / 32];
+      for (int nb = 0; nb < NB; ++nb) {
+        if (need_mask) {
 #pragma unroll
-      for (int kb2 = 0; kb2 < kKeyTile / 32; ++kb2) {
-        s[kb2] = f32x16_t{};
-#pragma unroll
-        for (int ds = 0; ds < kD / 16; ++ds) {
-          const bf16x8_t ka =
-              *reinterpret_cast<const bf16x8_t*>(&Ks[(kb2 * 32 + col) * kKsStride + 16 * ds + 8 * half]);
-          s[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[nb][ds], s[kb2], 0, 0, 0);
-        }
-      }
-      // Scale, mask, tile max.
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb2 = 0; kb2 < kKeyTile / 32; ++kb2) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + kb2 * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          bool ok;
-          if (is_tree) {
-            ok = key < kend;
-            uint64_t word = 0;
-#pragma unroll
-            for (int w = 0; w < kMaskWords; ++w) word = (w == (key >> 6)) ? mk[nb][w] : word;
-            ok = ok && ((word >> (key & 63)) & 1ull);
-          } else {
-            ok = key < kend;
+          for (int r = 0; r < 16; ++r) {
+            const int kk = kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);   // key within the tile
+            const bool ok = k0 + kk < kend && (!is_tree || ((mword[nb] >> kk) & 1ull));
+            s[nb][r] = ok ? s[nb][r] : -INFINITY;
           }
-          const float z = ok ? s[kb2][r] * a.scale_log2 : -INFINITY;
-          s[kb2][r] = z;
-          mx = fmaxf(mx, z);
         }
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      const float m_new = fmaxf(m_run[nb], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f(m_run[nb] - m_use);
-      m_run[nb] = m_new;
-      float psum = 0.f;
+        float mx = s[nb][0];
 #pragma unroll
-      for (int kb2 = 0; kb2 < kKeyTile / 32; ++kb2)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float pv = exp2f(s[kb2][r] - m_use);
-          s[kb2][r] = pv;
-          psum += pv;
+        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[nb][r]);
+        {
+          const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_int(mx), __float_as_int(mx), false, false);
+          mx = fmaxf(__int_as_float(sw2[0]), __int_as_float(sw2[1]));
         }
-      l_run[nb] = l_run[nb] * alpha + psum;
+        const float mt = mx * sl2;  // scale > 0, so the max commutes with scaling
+        if (__ballot(mt > m_run[nb] + kRescaleSlack)) {
+          const float m_new = fmaxf(m_run[nb], mt);
+          const float alpha = m_new == m_run[nb] ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
+          m_run[nb] = m_new;
+          l_run[nb] *= alpha;
 #pragma unroll
-      for (int db = 0; db < kD / 32; ++db) o[nb][db] *= alpha;
-
-      // O^T += V^T P^T, 16 keys per MFMA: B = P^T (regs 8*s2 .. 8*s2+7 of s[kb2]),
-      // A = V^T with the same key order: keys {16*s2 + 4*half + 0..3, 16*s2 + 8 + 4*half + 0..3}.
-#pragma unroll
-      for (int kb2 = 0; kb2 < kKeyTile / 32; ++kb2) {
+          for (int db = 0; db < kD / 32; ++db) o[nb][db] *= alpha;
+        }
+        const float m_use = m_run[nb] == -INFINITY ? 0.f : m_run[nb];
+        float psum = 0.f;
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
-          bf16x8_t pb;
+          bf16x8_t v;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) pb[i] = (__bf16)s[kb2][8 * s2 + i];
-          const int key_lo = kb2 * 32 + 16 * s2 + 4 * half;
-#pragma unroll
-          for (int db = 0; db < kD / 32; ++db) {
-            const uint16_t* vrow = &Vs[(db * 32 + col) * kVsStride];
-            const uint2 lo = *reinterpret_cast<const uint2*>(vrow + key_lo);
-            const uint2 hi = *reinterpret_cast<const uint2*>(vrow + key_lo + 8);
-            const bf16x8_t va = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-            o[nb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[nb][db], 0, 0, 0);
+          for (int i = 0; i < 8; i += 2) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(s[nb][8 * s2 + i], sl2, -m_use));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(s[nb][8 * s2 + i + 1], sl2, -m_use));
+            psum += p0 + p1;
+            const bf16x2_t pk = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
+            v[i] = pk[0];
+            v[i + 1] = pk[1];
           }
+          pb[nb][s2] = v;
         }
+        l_run[nb] += psum;
+      }
+
+      // O^T += V^T P^T over the 32 keys, 16 per MFMA.
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const uint8_t* vbase = lv + (kb * 32 + 16 * s2) * kRowBytes;
+        bf16x8_t va[kD / 32];
+#pragma unroll
+        for (int db = 0; db < kD / 32; ++db) {
+          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vbase + vofs[0][db]));
+          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vbase + vofs[1][db]));
+          const s16x8_t vv = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          va[db] = __builtin_bit_cast(bf16x8_t, vv);
+        }
+#pragma unroll
+        for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            o[nb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pb[nb][s2], o[nb][db], 0, 0, 0);
       }
     }
-    __syncthreads();
+    asm volatile("s_barrier" ::: "memory");  // every wave is done with this stage before it is refilled
   }
 
   // Epilogue: lane holds dims db*32 + 8*(r/4) + 4*half + r%4 of its query row.
@@ -264,9 +356,9 @@ __global__ __launch_bounds__((NB == 1 ? kMaxWaves : 4) * kWave) void tree_verify
   }
 }
 
-// One workgroup of D threads per stacked query row: merge the splits.
-__global__ __launch_bounds__(kD) void verify_combine_kernel(const VerifyArgs a) {
-  const int qr = blockIdx.x;
+// Merge the splits: 8 stacked rows per workgroup, 32 threads x 4 dims per row.
+__global__ __launch_bounds__(256) void verify_combine_kernel(const VerifyArgs a) {
+  const int qr = blockIdx.x * 8 + (threadIdx.x >> 5);
   const int bg = blockIdx.y;
   const int b = bg / a.Hkv;
   const int g = bg - b * a.Hkv;
@@ -274,23 +366,32 @@ __global__ __launch_bounds__(kD) void verify_combine_kernel(const VerifyArgs a) 
   if (qr >= T * a.G) return;
   const int u = qr / a.G;
   const int h = g * a.G + (qr - u * a.G);
-  const int dim = threadIdx.x;
+  const int dim = (threadIdx.x & 31) * 4;
   float M = -INFINITY;
   for (int s = 0; s < a.nsplit; ++s) {
     const float2 ml = a.ws_ml[((size_t)bg * a.nsplit + s) * a.rows_max + qr];
     if (ml.y > 0.f) M = fmaxf(M, ml.x);
   }
-  float num = 0.f, den = 0.f;
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  float den = 0.f;
   for (int s = 0; s < a.nsplit; ++s) {
     const size_t slot = ((size_t)bg * a.nsplit + s) * a.rows_max + qr;
     const float2 ml = a.ws_ml[slot];
     if (ml.y > 0.f) {
       const float w = exp2f(ml.x - M);
-      num += w * a.ws_o[slot * kD + dim];
+      const float4 v = *reinterpret_cast<const float4*>(a.ws_o + slot * kD + dim);
+      num.x += w * v.x;
+      num.y += w * v.y;
+      num.z += w * v.z;
+      num.w += w * v.w;
       den += w * ml.y;
     }
   }
-  a.out[(((size_t)b * a.T_max + u) * a.Hq + h) * kD + dim] = (uint16_t)f32_to_bf16_bits(num / den);
+  const float inv = 1.f / den;
+  uint2 pk;
+  pk.x = f32_to_bf16_bits(num.x * inv) | (f32_to_bf16_bits(num.y * inv) << 16);
+  pk.y = f32_to_bf16_bits(num.z * inv) | (f32_to_bf16_bits(num.w * inv) << 16);
+  *reinterpret_cast<uint2*>(a.out + (((size_t)b * a.T_max + u) * a.Hq + h) * kD + dim) = pk;
   if (dim == 0 && a.lse) a.lse[((size_t)b * a.Hq + h) * a.T_max + u] = (M + log2f(den)) * kLn2;
 }
 
@@ -300,18 +401,18 @@ VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv) {
   VerifyPlan p{};
   p.G = Hq / Hkv;
   p.rows_max = T_max * p.G;
-  p.nb = 2;
+  p.waves = kWaves;
   const int blocks = (p.rows_max + 31) / 32;
-  p.waves = std::min(4, std::max(1, (blocks + p.nb - 1) / p.nb));
-  if (blocks <= 4) {  // small trees: one block per wave keeps more waves busy
-    p.nb = 1;
-    p.waves = std::max(1, blocks);
-  }
-  p.rows_per_wg = p.waves * p.nb * 32;
+  // Two 32-row blocks per wave halve the LDS traffic per MFMA; one block per
+  // wave when two would add a whole row group of padding.
+  const int rg2 = (blocks + 2 * kWaves - 1) / (2 * kWaves);
+  const int rg1 = (blocks + kWaves - 1) / kWaves;
+  p.nb = (rg2 * 2 * kWaves - blocks) <= (rg1 * kWaves - blocks) + kWaves ? 2 : 1;
+  p.rows_per_wg = kWaves * p.nb * 32;
   p.rowgroups = (p.rows_max + p.rows_per_wg - 1) / p.rows_per_wg;
-  // Enough workgroups to cover 256 CUs twice, but splits no shorter than 512 keys.
-  const int base = B * Hkv * p.rowgroups;
-  const int want = std::max(1, (512 + base - 1) / std::max(base, 1));
+  // About one workgroup per CU (256 CUs), splits no shorter than 512 keys.
+  const int base = std::max(1, B * Hkv * p.rowgroups);
+  const int want = std::max(1, (256 + base - 1) / base);
   const int max_split = std::max(1, (L_stride + 511) / 512);
   p.nsplit = std::min(want, max_split);
   int chunk = (L_stride + p.nsplit - 1) / p.nsplit;
@@ -345,14 +446,13 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
   a.ws_ml = ws ? reinterpret_cast<float2*>(static_cast<char*>(ws) + slots * kD * sizeof(float)) : nullptr;
 
   const dim3 grid(p.nsplit, p.rowgroups, B * Hkv);
-  const dim3 block(p.waves * kWave);
   if (p.nb == 1)
-    hipLaunchKernelGGL(tree_verify_kernel<1>, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(tree_verify_kernel<1>, grid, dim3(kThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(tree_verify_kernel<2>, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(tree_verify_kernel<2>, grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.nsplit == 1) return e;
-  hipLaunchKernelGGL(verify_combine_kernel, dim3(p.rows_max, B * Hkv), dim3(kD), 0, stream, a);
+  hipLaunchKernelGGL(verify_combine_kernel, dim3((p.rows_max + 7) / 8, B * Hkv), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
