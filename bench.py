@@ -76,11 +76,12 @@ def main():
 
     import torch
     if args.copy_calibration:
+        # An elementwise kernel that reads and writes n bytes once each.
         n = args.copy_calibration << 20
-        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        src = torch.ones(n // 4, dtype=torch.int32, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(3):
-            dst.copy_(src)
+            torch.add(src, 1, out=dst)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "launches": 3}), flush=True)
         return

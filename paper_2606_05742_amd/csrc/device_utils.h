@@ -30,6 +30,26 @@ __device__ __forceinline__ float wave_sum_f32(float v) {
   return v;
 }
 
+// Sum over the wave without LDS traffic: DPP butterflies inside each row of 16
+// lanes (swap pairs, swap quads, half-row mirror, row mirror), then the four
+// row sums combined through scalar reads.  The order of additions is fixed,
+// so equal inputs give bit-equal sums; every lane returns the total.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  v += dpp_f32<0xb1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f32<0x4e>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f32<0x141>(v);  // row_half_mirror
+  v += dpp_f32<0x140>(v);  // row_mirror
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -99,6 +119,30 @@ __device__ __forceinline__ uint64_t topk_merge(uint64_t mine, uint64_t other) {
     c = low ? (c > p ? c : p) : (c < p ? c : p);
   }
   return c;
+}
+
+// Sort a wave-wide list of 64 keys descending (bitonic network).
+__device__ __forceinline__ uint64_t bitonic_sort_desc(uint64_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const uint64_t p = shfl_xor_u64(v, j);
+      const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
+      v = keep_max ? (v > p ? v : p) : (v < p ? v : p);
+    }
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint64_t p = shfl_xor_u64(v, off);
+    v = v > p ? v : p;
+  }
+  return v;
 }
 
 }  // namespace adapld

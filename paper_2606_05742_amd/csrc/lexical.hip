@@ -1,12 +1,15 @@
 // Lexical anchoring (Sec. 3.3): longest-suffix n-gram match over the context.
 //
-// One workgroup of 1024 threads (16 waves) per sequence.  Pass 1 computes, for
-// every candidate end position j in [0, L-2], the length of the common suffix
-// of M[..j] and M[..L-1] capped at n_max, and reduces its maximum n*.  Pass 2
-// re-derives the match lengths and compacts {j : len(j) >= n*} in ascending
-// order with wave ballots and a 16-entry workgroup scan.  The context is read
-// twice from L2 (a few KiB to 128 KiB per sequence), so the kernel is
-// latency-bound, not bandwidth-bound.
+// One workgroup of 1024 threads (16 waves) per sequence.  The context is
+// staged in LDS in pieces of up to kLexChunk tokens (plus the n_max-1 tokens
+// before each piece, so every n-gram ending in the piece is visible), with
+// 16-byte loads.  Pass 1 computes, for every candidate end position j in
+// [0, L-2], the length of the common suffix of M[..j] and M[..L-1] capped at
+// n_max, and reduces its maximum n*.  Pass 2 re-derives the match lengths,
+// each thread over a contiguous run of positions, and compacts
+// {j : len(j) >= n*} in ascending order with a wave scan and a 16-entry
+// workgroup scan of the per-thread hit counts.  A context that fits one piece
+// is staged once.
 #include "adapld_internal.h"
 #include "device_utils.h"
 
@@ -15,13 +18,29 @@ namespace {
 
 constexpr int kLexThreads = 1024;
 constexpr int kLexWaves = kLexThreads / kWave;
-constexpr int kMaxNmax = 64;
+constexpr int kMaxNmax = ADAPLD_MAX_NMAX;
+constexpr int kLexChunk = 16384;   // tokens per LDS piece (64 KiB)
+constexpr int kHalo = kMaxNmax;    // >= n_max - 1, multiple of 4
 
-__device__ __forceinline__ int suffix_len(const int32_t* __restrict__ M, const int* s_suffix,
-                                          int j, int cap) {
-  // cap = min(n_max, j + 1): the n-gram ending at j may not start before 0.
+// Stage tokens [lo, hi) at s_tok[kHalo - (p0 - lo) ...]: s_tok[kHalo + i] holds M[p0 + i].
+__device__ __forceinline__ void stage(const int32_t* __restrict__ M, int* s_tok, int p0, int lo, int hi) {
+  const int base = kHalo - (p0 - lo);  // LDS slot of token lo
+  const int n = hi - lo;
+  if (((lo | base) & 3) == 0 && (reinterpret_cast<uintptr_t>(M + lo) & 15) == 0) {
+    const int n4 = n >> 2;
+    for (int i = threadIdx.x; i < n4; i += kLexThreads)
+      *reinterpret_cast<int4*>(&s_tok[base + 4 * i]) = *reinterpret_cast<const int4*>(M + lo + 4 * i);
+    for (int i = 4 * n4 + threadIdx.x; i < n; i += kLexThreads) s_tok[base + i] = M[lo + i];
+  } else {
+    for (int i = threadIdx.x; i < n; i += kLexThreads) s_tok[base + i] = M[lo + i];
+  }
+}
+
+// Common-suffix length of M[..j] and the query suffix, capped at cap
+// (cap <= j + 1, so the n-gram never starts before position 0).
+__device__ __forceinline__ int suffix_len(const int* s_tok, int p0, const int* s_suffix, int j, int cap) {
   int n = 0;
-  while (n < cap && M[j - n] == s_suffix[n]) ++n;
+  while (n < cap && s_tok[kHalo + (j - p0) - n] == s_suffix[n]) ++n;
   return n;
 }
 
@@ -29,9 +48,9 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
     const int32_t* __restrict__ tokens, const int32_t* __restrict__ lens, int L_stride, int n_max,
     int32_t* __restrict__ cand_pos, int32_t* __restrict__ cand_count,
     int32_t* __restrict__ match_n) {
+  __shared__ __attribute__((aligned(16))) int s_tok[kHalo + kLexChunk];
   __shared__ int s_suffix[kMaxNmax];
   __shared__ int s_red[kLexWaves];
-  __shared__ int s_base[kLexWaves];
 
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -39,13 +58,22 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
   const int wave = tid / kWave;
   const int32_t* __restrict__ M = tokens + (size_t)b * L_stride;
   const int L = min(max(lens[b], 0), L_stride);
+  const int J = L - 1;  // candidate end positions are [0, J)
 
   if (tid < n_max && tid < L) s_suffix[tid] = M[L - 1 - tid];
-  __syncthreads();
+  const int npieces = J > 0 ? (J + kLexChunk - 1) / kLexChunk : 0;
 
   // Pass 1: n* = max over j of the capped common-suffix length.
   int best = 0;
-  for (int j = tid; j < L - 1; j += kLexThreads) best = max(best, suffix_len(M, s_suffix, j, min(n_max, j + 1)));
+  for (int p = 0; p < npieces; ++p) {
+    const int p0 = p * kLexChunk;
+    const int p1 = min(p0 + kLexChunk, J);
+    __syncthreads();
+    stage(M, s_tok, p0, max(p0 - (n_max - 1), 0), p1);
+    __syncthreads();
+    for (int j = p0 + tid; j < p1; j += kLexThreads)
+      best = max(best, suffix_len(s_tok, p0, s_suffix, j, min(n_max, j + 1)));
+  }
   best = wave_max_i32(best);
   if (lane == 0) s_red[wave] = best;
   __syncthreads();
@@ -57,23 +85,47 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
   int total = 0;
   if (n_star > 0) {
     int32_t* __restrict__ out = cand_pos + (size_t)b * L_stride;
-    for (int base = 0; base < L - 1; base += kLexThreads) {
-      const int j = base + tid;
-      bool hit = false;
-      if (j < L - 1 && j >= n_star - 1) hit = suffix_len(M, s_suffix, j, n_star) == n_star;
-      const uint64_t ball = __ballot(hit);
-      __syncthreads();  // previous round's s_base reads are done
-      if (lane == 0) s_base[wave] = __popcll(ball);
+    for (int p = 0; p < npieces; ++p) {
+      const int p0 = p * kLexChunk;
+      const int p1 = min(p0 + kLexChunk, J);
+      if (npieces > 1) {
+        __syncthreads();
+        stage(M, s_tok, p0, max(p0 - (n_max - 1), 0), p1);
+        __syncthreads();
+      }
+      // Thread tid owns the contiguous run [q0, q0 + per) of this piece, so one
+      // wave scan plus one workgroup scan of the hit counts orders all hits.
+      const int per = (p1 - p0 + kLexThreads - 1) / kLexThreads;  // <= kLexChunk / kLexThreads
+      const int q0 = p0 + tid * per;
+      uint32_t bits = 0;
+      for (int e = 0; e < per; ++e) {
+        const int j = q0 + e;
+        if (j < p1 && j >= n_star - 1 && suffix_len(s_tok, p0, s_suffix, j, n_star) == n_star) bits |= 1u << e;
+      }
+      const int cnt = __popc(bits);
+      int incl = cnt;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int v = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += v;
+      }
+      __syncthreads();  // earlier reads of s_red are done
+      if (lane == kWave - 1) s_red[wave] = incl;
       __syncthreads();
-      int before = 0, round_total = 0;
+      int before = 0, piece_total = 0;
 #pragma unroll
       for (int w = 0; w < kLexWaves; ++w) {
-        const int c = s_base[w];
+        const int c = s_red[w];
         before += (w < wave) ? c : 0;
-        round_total += c;
+        piece_total += c;
       }
-      if (hit) out[total + before + __popcll(ball & lanes_below())] = j;
-      total += round_total;
+      int slot = total + before + incl - cnt;
+      while (bits) {
+        const int e = __ffs(bits) - 1;
+        bits &= bits - 1;
+        out[slot++] = q0 + e;
+      }
+      total += piece_total;
     }
   }
   if (tid == 0) {

@@ -26,16 +26,16 @@ __global__ __launch_bounds__(kWave) void build_draft_tree_kernel(
   const int lane = lane_id();
   const int L = min(max(lens[b], 0), L_stride);
   const int32_t* __restrict__ M = tokens + (size_t)b * L_stride;
+  // The counts and the ranked positions are independent loads (entries past the
+  // count are read but not used).
   int cnt = min(max(topk_count[b], 0), k);
-  if (kind[b] == ADAPLD_KIND_NONE) cnt = 0;
+  const int kd = kind[b];
+  int r = lane < k ? topk_pos[(size_t)b * k + lane] : -1;
+  if (kd == ADAPLD_KIND_NONE) cnt = 0;
 
-  int r = -1, tok = -1;
-  bool valid = false;
-  if (lane < cnt) {
-    r = topk_pos[(size_t)b * k + lane];
-    valid = r >= 0 && r <= L - 2;
-    if (valid) tok = M[r + 1];
-  }
+  int tok = -1;
+  const bool valid = lane < cnt && r >= 0 && r <= L - 2;
+  if (valid) tok = M[r + 1];
   // A lane is a new branch if no lower valid lane holds the same successor token.
   bool dup = false;
   for (int j = 0; j < cnt; ++j) {

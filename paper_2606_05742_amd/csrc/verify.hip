@@ -4,7 +4,7 @@
 // Work decomposition.  For one sequence b and kv head g the T*G query rows
 // (node u, query head g*G + i) are stacked as row = u*G + i, so the G heads
 // that share a kv head share every K/V byte read from HBM.  A workgroup of 4
-// waves (one per SIMD) owns 4*NB*32 stacked rows and one split of the context
+// or 8 waves owns waves*NB*32 stacked rows and one split of the context
 // keys; the last split also takes the tree keys.  Grid = (splits, row groups,
 // B*Hkv).
 //
@@ -28,6 +28,7 @@
 // Splits write unnormalised partial outputs with their running max and sum to
 // the workspace; a combine kernel merges them with log-sum-exp weights.
 #include <algorithm>
+#include <type_traits>
 
 #include "adapld_internal.h"
 #include "device_utils.h"
@@ -43,20 +44,18 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x8_t __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
 
 constexpr int kD = ADAPLD_HEAD_DIM;           // 128 bf16 = 256 bytes per key row
 constexpr int kRowBytes = kD * 2;
-constexpr int kWaves = 4;
-constexpr int kThreads = kWaves * kWave;
 constexpr int kStages = 3;
 constexpr int kTileBytes = kKeyTile * kRowBytes;  // 16 KiB for K (and for V)
-constexpr int kLoadsPerWave = 2 * kTileBytes / 1024 / kWaves;  // 1 KiB per wave-wide load
 constexpr int kMaskWords = (ADAPLD_MAX_TREE_NODES + 63) / 64;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleSlack = 8.0f;         // log2 units the running max may lag
 
-static_assert(kLoadsPerWave == 8, "the vmcnt values in wait_tile_and_sync assume 8 loads per wave per tile");
 
 struct VerifyArgs {
   const uint16_t* q;
@@ -67,7 +66,7 @@ struct VerifyArgs {
   const int32_t* lens;
   const int32_t* node_count;
   const uint64_t* tree_mask;
-  int L_stride, T_max, Hq, Hkv, G, rows_max, nsplit, chunk, nw;
+  int L_stride, T_max, Hq, Hkv, G, rows_max, nsplit, chunk, nw, rowgroups, n_kvgroups;
   float scale_log2;
   uint16_t* out;
   float* lse;
@@ -101,15 +100,17 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
                : "memory", "m0");
 }
 
-// Issue this wave's share of one K/V tile: rows [16*wave, 16*wave + 16) of K and
-// of V, four rows (1 KiB) per instruction.  Keys past kend re-read key kend-1
-// (in bounds); their logits are masked.
+// Issue this wave's share of one K/V tile: 64/WAVES key rows of K and of V,
+// four rows (1 KiB) per instruction.  Keys past kend re-read key kend-1 (in
+// bounds); their logits are masked.
+template <int WAVES>
 __device__ __forceinline__ void issue_tile(const uint16_t* kb, const uint16_t* vb, size_t stride,
                                            int k0, int kend, uint32_t lk, uint32_t lv, int wave,
                                            int lane) {
+  constexpr int kRowsPerWave = kKeyTile / WAVES;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row0 = 16 * wave + 4 * i;
+  for (int i = 0; i < kRowsPerWave / 4; ++i) {
+    const int row0 = kRowsPerWave * wave + 4 * i;
     const int row = row0 + (lane >> 4);
     const int c = (lane & 15) ^ swz(row);
     const size_t key = (size_t)min(k0 + row, kend - 1);
@@ -120,29 +121,43 @@ __device__ __forceinline__ void issue_tile(const uint16_t* kb, const uint16_t* v
 }
 
 // Wait for this wave's loads of the current tile, then for every wave's (the
-// barrier).  The asm memory clobber keeps LDS reads from moving above it.
+// barrier).  LPW = loads per wave per tile; `later` tiles issued after the
+// current one may stay in flight.  The asm memory clobber keeps LDS reads from
+// moving above it.
+template <int LPW>
 __device__ __forceinline__ void wait_tile_and_sync(int later) {
-  if (later >= 2) asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
-  else if (later == 1) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+  static_assert(2 * LPW < 64, "vmcnt holds 6 bits");
+  if (later >= 2) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * LPW) : "memory");
+  else if (later == 1) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(LPW) : "memory");
   else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int NB>
-__global__ __launch_bounds__(kThreads, 1) void tree_verify_kernel(const VerifyArgs a) {
+template <int NB, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const VerifyArgs a) {
+  constexpr int kThreads = WAVES * kWave;
+  constexpr int kLoadsPerWave = 2 * kTileBytes / 1024 / WAVES;   // 1 KiB per wave-wide load
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * 2 * kTileBytes];
   __shared__ uint64_t s_mask[ADAPLD_MAX_TREE_NODES * kMaskWords];
 
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int split = blockIdx.x;
-  const int bg = blockIdx.z;
+  // Workgroups are dispatched round-robin over the 8 XCDs; the row groups of
+  // one (kv head, split) get consecutive slots on the same XCD, so the second
+  // reader of a K/V tile finds it in that XCD's L2.
+  const int xcd = blockIdx.x & 7;
+  const int slot = blockIdx.x >> 3;
+  const int kvgroup = (slot / a.rowgroups) * 8 + xcd;   // = bg * nsplit + split
+  const int rg = slot % a.rowgroups;
+  if (kvgroup >= a.n_kvgroups) return;
+  const int bg = kvgroup / a.nsplit;
+  const int split = kvgroup - bg * a.nsplit;
   const int b = bg / a.Hkv;
   const int g = bg - b * a.Hkv;
   const int T = min(max(a.node_count[b], 0), a.T_max);
   const int L = min(max(a.lens[b], 0), a.L_stride);
   const int G = a.G;
   const int rows = T * G;
-  const int row_base = blockIdx.y * (kWaves * NB * 32);
+  const int row_base = rg * (WAVES * NB * 32);
   if (row_base >= rows) return;
 
   const int c0 = split * a.chunk;
@@ -189,26 +204,21 @@ __global__ __launch_bounds__(kThreads, 1) void tree_verify_kernel(const VerifyAr
   const uint16_t* vc = a.v_ctx + (size_t)bg * a.L_stride * kD;
   const size_t tree_off = ((size_t)b * a.T_max * a.Hkv + g) * kD;
   const size_t tree_stride = (size_t)a.Hkv * kD;
-
   const uint32_t smem_base = lds_addr(smem);
+
   auto issue = [&](int t) {
     const uint32_t lk = smem_base + (t % kStages) * 2 * kTileBytes;
     if (t < n_ctx)
-      issue_tile(kc, vc, kD, c0 + t * kKeyTile, c1, lk, lk + kTileBytes, wave, lane);
+      issue_tile<WAVES>(kc, vc, kD, c0 + t * kKeyTile, c1, lk, lk + kTileBytes, wave, lane);
     else
-      issue_tile(a.k_tree + tree_off, a.v_tree + tree_off, tree_stride, (t - n_ctx) * kKeyTile, T, lk,
-                 lk + kTileBytes, wave, lane);
+      issue_tile<WAVES>(a.k_tree + tree_off, a.v_tree + tree_off, tree_stride, (t - n_ctx) * kKeyTile, T,
+                        lk, lk + kTileBytes, wave, lane);
   };
 
-#pragma unroll
-  for (int t = 0; t < kStages - 1; ++t)
-    if (t < n_tiles) issue(t);
-
-  const float sl2 = a.scale_log2;
   // Lane-dependent LDS byte offsets within a stage.  K fragment for dims
-  // [16*ds + 8*half, +8) of key row kb*32 + col: kofs[ds] + kb*32*kRowBytes.
-  // Transposed V reads: each 16-lane group covers 4 keys x 16 dims; the key
-  // rows are kb*32 + 16*s2 + vkey (+8), whose swizzle depends on vkey only.
+  // [16*ds + 8*half, +8) of key row kb*32 + col sits at kofs[ds] + kb*32*kRowBytes.
+  // Transposed V reads: each 16-lane group covers 4 keys x 16 dims; the key rows
+  // are kb*32 + 16*s2 + vkey (+8), whose swizzle depends on vkey only.
   int kofs[kD / 16];
 #pragma unroll
   for (int ds = 0; ds < kD / 16; ++ds) kofs[ds] = col * kRowBytes + (((2 * ds + half) ^ swz(col)) << 4);
@@ -221,30 +231,42 @@ __global__ __launch_bounds__(kThreads, 1) void tree_verify_kernel(const VerifyAr
     vofs[0][db] = vkey * kRowBytes + ((cch ^ swz(vkey)) << 4) + (vdim & 7) * 2;
     vofs[1][db] = (vkey + 8) * kRowBytes + ((cch ^ swz(vkey + 8)) << 4) + (vdim & 7) * 2;
   }
+  const float sl2 = a.scale_log2;
+
+#pragma unroll
+  for (int t = 0; t < kStages - 1; ++t)
+    if (t < n_tiles) issue(t);
+
   for (int t = 0; t < n_tiles; ++t) {
     if (t + kStages - 1 < n_tiles) issue(t + kStages - 1);
-    wait_tile_and_sync(min(kStages - 1, n_tiles - 1 - t));
-    const uint8_t* lk = smem + (t % kStages) * 2 * kTileBytes;
-    const uint8_t* lv = lk + kTileBytes;
+    wait_tile_and_sync<kLoadsPerWave>(min(kStages - 1, n_tiles - 1 - t));
+    // Per-tile lane addresses (32-bit LDS pointers); the half and step offsets
+    // below are instruction immediates.
+    const lds_u8* lk = (const lds_u8*)smem + (t % kStages) * 2 * kTileBytes;
+    const lds_u8* lv = lk + kTileBytes;
+    const lds_u8* kp[kD / 16];
+#pragma unroll
+    for (int ds = 0; ds < kD / 16; ++ds) kp[ds] = lk + kofs[ds];
+    const lds_u8* vp[2][kD / 32];
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db) {
+      vp[0][db] = lv + vofs[0][db];
+      vp[1][db] = lv + vofs[1][db];
+    }
     const bool is_tree = t >= n_ctx;
     const int k0 = is_tree ? (t - n_ctx) * kKeyTile : c0 + t * kKeyTile;
     const int kend = is_tree ? T : c1;
     const bool need_mask = is_tree || k0 + kKeyTile > kend;
-    uint64_t mword[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      mword[nb] = (is_tree && qrow[nb] < rows) ? s_mask[qu[nb] * a.nw + (k0 >> 6)] : 0ull;
 
-#pragma unroll 1   // unrolling lets the scheduler overlap the halves and spill
+#pragma unroll 1   // unrolled halves interleave under the scheduler and spill
     for (int kb = 0; kb < 2; ++kb) {
       // S^T for 32 keys; each K fragment feeds NB query blocks.
       f32x16_t s[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) s[nb] = f32x16_t{};
-      const uint8_t* kbase = lk + kb * 32 * kRowBytes;
 #pragma unroll
       for (int ds = 0; ds < kD / 16; ++ds) {
-        const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(kbase + kofs[ds]);
+        const bf16x8_t ka = *reinterpret_cast<const lds_bf16x8_t*>(kp[ds] + kb * 32 * kRowBytes);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
           s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[nb][ds], s[nb], 0, 0, 0);
@@ -255,16 +277,18 @@ __global__ __launch_bounds__(kThreads, 1) void tree_verify_kernel(const VerifyAr
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         if (need_mask) {
+          const uint64_t mword = (is_tree && qrow[nb] < rows) ? s_mask[qu[nb] * a.nw + (k0 >> 6)] : 0ull;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int kk = kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);   // key within the tile
-            const bool ok = k0 + kk < kend && (!is_tree || ((mword[nb] >> kk) & 1ull));
+            const bool ok = k0 + kk < kend && (!is_tree || ((mword >> kk) & 1ull));
             s[nb][r] = ok ? s[nb][r] : -INFINITY;
           }
         }
-        float mx = s[nb][0];
+        float mx = fmaxf(fmaxf(s[nb][0], s[nb][1]), s[nb][2]);
 #pragma unroll
-        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[nb][r]);
+        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[nb][r]), s[nb][r + 1]);
+        mx = fmaxf(mx, s[nb][15]);
         {
           const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_int(mx), __float_as_int(mx), false, false);
           mx = fmaxf(__int_as_float(sw2[0]), __int_as_float(sw2[1]));
@@ -300,20 +324,17 @@ __global__ __launch_bounds__(kThreads, 1) void tree_verify_kernel(const VerifyAr
       // O^T += V^T P^T over the 32 keys, 16 per MFMA.
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        const uint8_t* vbase = lv + (kb * 32 + 16 * s2) * kRowBytes;
-        bf16x8_t va[kD / 32];
 #pragma unroll
         for (int db = 0; db < kD / 32; ++db) {
-          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vbase + vofs[0][db]));
-          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vbase + vofs[1][db]));
+          const int off = (kb * 32 + 16 * s2) * kRowBytes;
+          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vp[0][db] + off));
+          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vp[1][db] + off));
           const s16x8_t vv = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          va[db] = __builtin_bit_cast(bf16x8_t, vv);
-        }
-#pragma unroll
-        for (int db = 0; db < kD / 32; ++db)
+          const bf16x8_t va = __builtin_bit_cast(bf16x8_t, vv);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
-            o[nb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pb[nb][s2], o[nb][db], 0, 0, 0);
+            o[nb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[nb][s2], o[nb][db], 0, 0, 0);
+        }
       }
     }
     asm volatile("s_barrier" ::: "memory");  // every wave is done with this stage before it is refilled
@@ -401,14 +422,12 @@ VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv) {
   VerifyPlan p{};
   p.G = Hq / Hkv;
   p.rows_max = T_max * p.G;
-  p.waves = kWaves;
+  // 8 waves x one 32-row block (two waves per SIMD, so one wave's softmax and
+  // LDS waits overlap the other's MFMAs); small trees use 4 waves.
   const int blocks = (p.rows_max + 31) / 32;
-  // Two 32-row blocks per wave halve the LDS traffic per MFMA; one block per
-  // wave when two would add a whole row group of padding.
-  const int rg2 = (blocks + 2 * kWaves - 1) / (2 * kWaves);
-  const int rg1 = (blocks + kWaves - 1) / kWaves;
-  p.nb = (rg2 * 2 * kWaves - blocks) <= (rg1 * kWaves - blocks) + kWaves ? 2 : 1;
-  p.rows_per_wg = kWaves * p.nb * 32;
+  p.nb = 1;
+  p.waves = blocks > 4 ? 8 : 4;
+  p.rows_per_wg = p.waves * p.nb * 32;
   p.rowgroups = (p.rows_max + p.rows_per_wg - 1) / p.rows_per_wg;
   // About one workgroup per CU (256 CUs), splits no shorter than 512 keys.
   const int base = std::max(1, B * Hkv * p.rowgroups);
@@ -445,11 +464,13 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
   a.ws_o = static_cast<float*>(ws);
   a.ws_ml = ws ? reinterpret_cast<float2*>(static_cast<char*>(ws) + slots * kD * sizeof(float)) : nullptr;
 
-  const dim3 grid(p.nsplit, p.rowgroups, B * Hkv);
-  if (p.nb == 1)
-    hipLaunchKernelGGL(tree_verify_kernel<1>, grid, dim3(kThreads), 0, stream, a);
+  a.rowgroups = p.rowgroups;
+  a.n_kvgroups = B * Hkv * p.nsplit;
+  const dim3 grid(((a.n_kvgroups + 7) / 8) * 8 * p.rowgroups);
+  if (p.waves == 8)
+    hipLaunchKernelGGL((tree_verify_kernel<1, 8>), grid, dim3(8 * kWave), 0, stream, a);
   else
-    hipLaunchKernelGGL(tree_verify_kernel<2>, grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((tree_verify_kernel<1, 4>), grid, dim3(4 * kWave), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.nsplit == 1) return e;
   hipLaunchKernelGGL(verify_combine_kernel, dim3((p.rows_max + 7) / 8, B * Hkv), dim3(256), 0, stream, a);
