@@ -207,8 +207,11 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
  *   lse        fp32 [B, Hq, T_max]     (out, may be NULL) entries u >= T not written
  *   ws         workspace of adapld_workspace_bytes(ADAPLD_OP_TREE_VERIFY_ATTN, B, L_stride, 0, 0, T_max, Hq, Hkv, D)
  *
+ * q, k and v must be finite (NaN or infinite inputs give undefined results);
+ * scale must be finite and > 0 (the usual 1/sqrt(D)).
+ *
  * Errors: NULL_ARG; INVALID_ARG for Hq % Hkv != 0, non-positive sizes,
- * non-finite scale or misaligned pointers; UNSUPPORTED for D != 128 or
+ * scale not finite and > 0, or misaligned pointers; UNSUPPORTED for D != 128 or
  * T_max > ADAPLD_MAX_TREE_NODES; WORKSPACE_TOO_SMALL.
  */
 int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx,

@@ -123,7 +123,8 @@ int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint
   if (B == 0) return ADAPLD_OK;
   if (!q || !k_ctx || !v_ctx || !k_tree || !v_tree || !lens || !node_count || !tree_mask || !out)
     return ADAPLD_ERR_NULL_ARG;
-  if (L_stride < 1 || T_max < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || !std::isfinite(scale))
+  if (L_stride < 1 || T_max < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || !std::isfinite(scale) ||
+      !(scale > 0.f))
     return ADAPLD_ERR_INVALID_ARG;
   if (D != ADAPLD_HEAD_DIM || T_max > ADAPLD_MAX_TREE_NODES) return ADAPLD_ERR_UNSUPPORTED;
   if (misaligned16(q) || misaligned16(k_ctx) || misaligned16(v_ctx) || misaligned16(k_tree) ||

@@ -5,14 +5,15 @@
 // (node u, query head g*G + i) are stacked as row = u*G + i, so the G heads
 // that share a kv head share every K/V byte read from HBM.  A workgroup of 4
 // or 8 waves owns waves*NB*32 stacked rows and one split of the context
-// keys; the last split also takes the tree keys.  Grid = (splits, row groups,
-// B*Hkv).
+// keys; the last split also takes the tree keys.  The grid is one-dimensional
+// and XCD-aware (see the block index decode in the kernel).
 //
-// Memory pipeline.  K and V tiles of 64 keys stream through a 3-stage LDS ring
-// with direct-to-LDS loads (global_load_lds_dwordx4): no VGPR staging, and two
-// tiles are in flight while the third is consumed.  Each 256-byte key row is
-// stored with its 16-byte chunks XOR-swizzled by the row index, which keeps
-// both LDS read patterns below free of bank conflicts.
+// Memory pipeline.  K and V tiles of 64 keys stream through a 4-stage LDS ring
+// with direct-to-LDS loads (global_load_lds_dwordx4): no VGPR staging, and up
+// to three tiles are in flight.  Each 256-byte key row is stored with its
+// 16-byte chunks XOR-swizzled by the row index, which keeps both LDS read
+// patterns below free of bank conflicts.  One barrier per tile both publishes
+// the next tile and frees the stage of the tile before the current one.
 //
 // Math.  S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (A = K rows read from LDS,
 // B = the wave's query block held in registers) leaves every lane owning one
@@ -24,6 +25,13 @@
 // needed.  Logits are fp32 in the log2 domain; the running max is only moved
 // when it grows by more than 8 (a factor 256), which keeps the rescale of the
 // output accumulators off the common path.
+//
+// Schedule.  The loop is software-pipelined over half tiles of 32 keys: the
+// MFMAs of P V for half h-1 are issued beside the max of half h, and those of
+// S for half h+1 beside the exponentials of half h, so each wave keeps its
+// matrix core busy while its softmax runs on the VALU.  Tiles with a masked
+// key (the ragged end of the context and the tree tiles) run the same
+// pipeline with the mask applied.
 //
 // Splits write unnormalised partial outputs with their running max and sum to
 // the workspace; a combine kernel merges them with log-sum-exp weights.
@@ -49,7 +57,7 @@ typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
 
 constexpr int kD = ADAPLD_HEAD_DIM;           // 128 bf16 = 256 bytes per key row
 constexpr int kRowBytes = kD * 2;
-constexpr int kStages = 3;
+constexpr int kStages = 4;  // power of two
 constexpr int kTileBytes = kKeyTile * kRowBytes;  // 16 KiB for K (and for V)
 constexpr int kMaskWords = (ADAPLD_MAX_TREE_NODES + 63) / 64;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -127,9 +135,9 @@ __device__ __forceinline__ void issue_tile(const uint16_t* kb, const uint16_t* v
 template <int LPW>
 __device__ __forceinline__ void wait_tile_and_sync(int later) {
   static_assert(2 * LPW < 64, "vmcnt holds 6 bits");
-  if (later >= 2) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * LPW) : "memory");
-  else if (later == 1) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(LPW) : "memory");
-  else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  if (later >= 2) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * LPW) : "memory");
+  else if (later == 1) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LPW) : "memory");
+  else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 template <int NB, int WAVES>
@@ -233,111 +241,123 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   }
   const float sl2 = a.scale_log2;
 
+  static_assert(NB == 1, "software-pipelined loop handles one 32-row block per wave");
+  // Half h covers keys [32*(h&1), +32) of tile h>>1, which sits in stage (h>>1) % kStages.
+  auto stage_of = [&](int h) { return (const lds_u8*)smem + ((h >> 1) & (kStages - 1)) * 2 * kTileBytes; };
+  auto qk = [&](int h, f32x16_t& sacc) {
+    const lds_u8* kbase = stage_of(h) + (h & 1) * 32 * kRowBytes;
+    sacc = f32x16_t{};
+#pragma unroll
+    for (int ds = 0; ds < kD / 16; ++ds) {
+      const bf16x8_t ka = *reinterpret_cast<const lds_bf16x8_t*>(kbase + kofs[ds]);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[0][ds], sacc, 0, 0, 0);
+    }
+  };
+  auto pv = [&](int h, const bf16x8_t (&pbv)[2]) {
+    const lds_u8* vbase = stage_of(h) + kTileBytes + (h & 1) * 32 * kRowBytes;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db) {
+        const lds_u8* vb2 = vbase + 16 * s2 * kRowBytes;
+        const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vb2 + vofs[0][db]));
+        const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vb2 + vofs[1][db]));
+        const s16x8_t vv = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv), pbv[s2], o[0][db], 0, 0, 0);
+      }
+    }
+  };
+  // Mask (masked tiles only), row max, and the lazy rescale of the running state.
+  auto max_rescale = [&](int h, f32x16_t& sv, auto masked) {
+    if constexpr (decltype(masked)::value) {
+      const int t = h >> 1, kb = h & 1;
+      const bool is_tree = t >= n_ctx;
+      const int k0 = is_tree ? (t - n_ctx) * kKeyTile : c0 + t * kKeyTile;
+      const int kend = is_tree ? T : c1;
+      const uint64_t mword = (is_tree && qrow[0] < rows) ? s_mask[qu[0] * a.nw + (k0 >> 6)] : 0ull;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kk = kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);   // key within the tile
+        const bool ok = k0 + kk < kend && (!is_tree || ((mword >> kk) & 1ull));
+        sv[r] = ok ? sv[r] : -INFINITY;
+      }
+    }
+    float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
+#pragma unroll
+    for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sv[r]), sv[r + 1]);
+    mx = fmaxf(mx, sv[15]);
+    {
+      const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_int(mx), __float_as_int(mx), false, false);
+      mx = fmaxf(__int_as_float(sw2[0]), __int_as_float(sw2[1]));
+    }
+    const float mt = mx * sl2;  // scale > 0, so the max commutes with scaling
+    if (__ballot(mt > m_run[0] + kRescaleSlack)) {
+      const float m_new = fmaxf(m_run[0], mt);
+      const float alpha = m_new == m_run[0] ? 1.f : __builtin_amdgcn_exp2f(m_run[0] - m_new);
+      m_run[0] = m_new;
+      l_run[0] *= alpha;
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db) o[0][db] *= alpha;
+    }
+  };
+  // P = exp2(S*scale - m) packed to bf16 in MFMA B-operand order.
+  auto exp_pack = [&](const f32x16_t& sv, bf16x8_t (&pbv)[2]) {
+    const float m_use = m_run[0] == -INFINITY ? 0.f : m_run[0];
+    float psum = 0.f;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      bf16x8_t v;
+#pragma unroll
+      for (int i = 0; i < 8; i += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[8 * s2 + i], sl2, -m_use));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[8 * s2 + i + 1], sl2, -m_use));
+        psum += p0 + p1;
+        const bf16x2_t pk = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
+        v[i] = pk[0];
+        v[i + 1] = pk[1];
+      }
+      pbv[s2] = v;
+    }
+    l_run[0] += psum;
+  };
+  // Before the first half of tile t+1: wait for its loads, then the barrier.
+  // Every wave has passed the last read of tile t-1 by then, so its stage is
+  // refilled with tile t+kStages-1.
+  auto next_tile = [&](int t) {
+    wait_tile_and_sync<kLoadsPerWave>(min(kStages - 3, n_tiles - 2 - t));
+    if (t + kStages - 1 < n_tiles) issue(t + kStages - 1);
+  };
+
+  // Software pipeline over halves: while the softmax of half h runs on the
+  // VALU, the MFMAs of PV(h-1) and of S(h+1) are in flight.
+  const int H = 2 * n_tiles;
+  const int n_plain = max(c1 - c0, 0) / kKeyTile;   // leading context tiles with no masked key
+  const int H_plain = 2 * n_plain;
 #pragma unroll
   for (int t = 0; t < kStages - 1; ++t)
     if (t < n_tiles) issue(t);
-
-  for (int t = 0; t < n_tiles; ++t) {
-    if (t + kStages - 1 < n_tiles) issue(t + kStages - 1);
-    wait_tile_and_sync<kLoadsPerWave>(min(kStages - 1, n_tiles - 1 - t));
-    // Per-tile lane addresses (32-bit LDS pointers); the half and step offsets
-    // below are instruction immediates.
-    const lds_u8* lk = (const lds_u8*)smem + (t % kStages) * 2 * kTileBytes;
-    const lds_u8* lv = lk + kTileBytes;
-    const lds_u8* kp[kD / 16];
-#pragma unroll
-    for (int ds = 0; ds < kD / 16; ++ds) kp[ds] = lk + kofs[ds];
-    const lds_u8* vp[2][kD / 32];
-#pragma unroll
-    for (int db = 0; db < kD / 32; ++db) {
-      vp[0][db] = lv + vofs[0][db];
-      vp[1][db] = lv + vofs[1][db];
-    }
-    const bool is_tree = t >= n_ctx;
-    const int k0 = is_tree ? (t - n_ctx) * kKeyTile : c0 + t * kKeyTile;
-    const int kend = is_tree ? T : c1;
-    const bool need_mask = is_tree || k0 + kKeyTile > kend;
-
-#pragma unroll 1   // unrolled halves interleave under the scheduler and spill
-    for (int kb = 0; kb < 2; ++kb) {
-      // S^T for 32 keys; each K fragment feeds NB query blocks.
-      f32x16_t s[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) s[nb] = f32x16_t{};
-#pragma unroll
-      for (int ds = 0; ds < kD / 16; ++ds) {
-        const bf16x8_t ka = *reinterpret_cast<const lds_bf16x8_t*>(kp[ds] + kb * 32 * kRowBytes);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[nb][ds], s[nb], 0, 0, 0);
-      }
-
-      // Online softmax; P packed to bf16 in MFMA B-operand order.
-      bf16x8_t pb[NB][2];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        if (need_mask) {
-          const uint64_t mword = (is_tree && qrow[nb] < rows) ? s_mask[qu[nb] * a.nw + (k0 >> 6)] : 0ull;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int kk = kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);   // key within the tile
-            const bool ok = k0 + kk < kend && (!is_tree || ((mword >> kk) & 1ull));
-            s[nb][r] = ok ? s[nb][r] : -INFINITY;
-          }
-        }
-        float mx = fmaxf(fmaxf(s[nb][0], s[nb][1]), s[nb][2]);
-#pragma unroll
-        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[nb][r]), s[nb][r + 1]);
-        mx = fmaxf(mx, s[nb][15]);
-        {
-          const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_int(mx), __float_as_int(mx), false, false);
-          mx = fmaxf(__int_as_float(sw2[0]), __int_as_float(sw2[1]));
-        }
-        const float mt = mx * sl2;  // scale > 0, so the max commutes with scaling
-        if (__ballot(mt > m_run[nb] + kRescaleSlack)) {
-          const float m_new = fmaxf(m_run[nb], mt);
-          const float alpha = m_new == m_run[nb] ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
-          m_run[nb] = m_new;
-          l_run[nb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < kD / 32; ++db) o[nb][db] *= alpha;
-        }
-        const float m_use = m_run[nb] == -INFINITY ? 0.f : m_run[nb];
-        float psum = 0.f;
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          bf16x8_t v;
-#pragma unroll
-          for (int i = 0; i < 8; i += 2) {
-            const float p0 = __builtin_amdgcn_exp2f(fmaf(s[nb][8 * s2 + i], sl2, -m_use));
-            const float p1 = __builtin_amdgcn_exp2f(fmaf(s[nb][8 * s2 + i + 1], sl2, -m_use));
-            psum += p0 + p1;
-            const bf16x2_t pk = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
-            v[i] = pk[0];
-            v[i + 1] = pk[1];
-          }
-          pb[nb][s2] = v;
-        }
-        l_run[nb] += psum;
-      }
-
-      // O^T += V^T P^T over the 32 keys, 16 per MFMA.
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-#pragma unroll
-        for (int db = 0; db < kD / 32; ++db) {
-          const int off = (kb * 32 + 16 * s2) * kRowBytes;
-          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vp[0][db] + off));
-          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vp[1][db] + off));
-          const s16x8_t vv = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          const bf16x8_t va = __builtin_bit_cast(bf16x8_t, vv);
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            o[nb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[nb][s2], o[nb][db], 0, 0, 0);
-        }
-      }
-    }
-    asm volatile("s_barrier" ::: "memory");  // every wave is done with this stage before it is refilled
+  if (H > 0) {
+    f32x16_t s_cur, s_nxt;
+    bf16x8_t pb[2];
+    wait_tile_and_sync<kLoadsPerWave>(min(kStages - 2, n_tiles - 1));
+    qk(0, s_cur);
+    if (H_plain > 0) max_rescale(0, s_cur, std::false_type{});
+    else max_rescale(0, s_cur, std::true_type{});
+    qk(1, s_nxt);
+    exp_pack(s_cur, pb);
+    s_cur = s_nxt;
+    auto body = [&](int h, auto masked) {
+      pv(h - 1, pb);
+      max_rescale(h, s_cur, masked);
+      if ((h & 1) && h + 1 < H) next_tile(h >> 1);
+      qk(h + 1, s_nxt);        // past the last half this reads a stale stage; unused
+      exp_pack(s_cur, pb);
+      s_cur = s_nxt;
+    };
+    int h = 1;
+    for (; h < H_plain; ++h) body(h, std::false_type{});
+    for (; h < H; ++h) body(h, std::true_type{});
+    pv(H - 1, pb);
   }
 
   // Epilogue: lane holds dims db*32 + 8*(r/4) + 4*half + r%4 of its query row.

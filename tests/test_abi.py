@@ -107,6 +107,8 @@ def test_verify_validation(lib):
     assert f(*args(D=64)) == UNSUPPORTED
     assert f(*args(T=300)) == UNSUPPORTED
     assert f(*args(scale=float("inf"))) == INVALID
+    assert f(*args(scale=0.0)) == INVALID
+    assert f(*args(scale=-0.1)) == INVALID
     assert f(*args(q=ctypes.c_void_p(0x10002))) == INVALID
     # L = 8192 splits the context, so a workspace is required
     assert lib.adapld_workspace_bytes(4, 2, 8192, 0, 0, 24, 8, 2, 128) > 0
