@@ -74,6 +74,7 @@ extern "C" {
 #define ADAPLD_MAX_HIDDEN 8192
 #define ADAPLD_MAX_TREE_NODES 256
 #define ADAPLD_HEAD_DIM 128
+#define ADAPLD_MAX_SEMANTIC_BATCH 2048   /* sequences per adapld_semantic_topk call */
 
 /* Human-readable text for a status code (static storage, never NULL). */
 const char* adapld_status_string(int status);
@@ -142,7 +143,8 @@ int adapld_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int 
  *   ws         workspace of adapld_workspace_bytes(ADAPLD_OP_SEMANTIC_TOPK, B, L_stride, d, k, ...)
  *
  * Errors: NULL_ARG; INVALID_ARG for bad sizes or misaligned bf16 pointers;
- * UNSUPPORTED for d or k beyond the limits; WORKSPACE_TOO_SMALL.
+ * UNSUPPORTED for d or k beyond the limits, B > ADAPLD_MAX_SEMANTIC_BATCH or
+ * B * L_stride > INT32_MAX; WORKSPACE_TOO_SMALL.
  */
 int adapld_semantic_topk(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
                          const int32_t* cand_pos, const int32_t* cand_count, int B, int L_stride,

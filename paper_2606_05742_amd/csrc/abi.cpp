@@ -20,7 +20,7 @@ int hip_status(hipError_t e) {
 }
 
 size_t semantic_ws(int B, int L_stride, int k) {
-  return (size_t)B * adapld::scan_chunks(L_stride) * k * sizeof(uint64_t);
+  return (size_t)B * adapld::scan_lists(L_stride) * k * sizeof(uint64_t);
 }
 
 }  // namespace
@@ -85,7 +85,9 @@ int adapld_semantic_topk(const uint16_t* bank, const uint16_t* query, const int3
       !kind || !ws)
     return ADAPLD_ERR_NULL_ARG;
   if (L_stride < 1 || d < 8 || d % 8 != 0 || k < 1) return ADAPLD_ERR_INVALID_ARG;
-  if (d > ADAPLD_MAX_HIDDEN || k > ADAPLD_MAX_K) return ADAPLD_ERR_UNSUPPORTED;
+  if (d > ADAPLD_MAX_HIDDEN || k > ADAPLD_MAX_K || B > ADAPLD_MAX_SEMANTIC_BATCH ||
+      (int64_t)B * L_stride > INT32_MAX)
+    return ADAPLD_ERR_UNSUPPORTED;
   if (misaligned16(bank) || (query && misaligned16(query))) return ADAPLD_ERR_INVALID_ARG;
   if (ws_bytes < semantic_ws(B, L_stride, k)) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
   return hip_status(adapld::launch_semantic_topk(bank, query, lens, cand_pos, cand_count, B,

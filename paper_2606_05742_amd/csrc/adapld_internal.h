@@ -14,17 +14,17 @@ namespace adapld {
 // Host-side shape decisions shared by the workspace query and the launchers,
 // so that both always agree.
 
-// Semantic scan: rows of one sequence are split into chunks of kRowsPerChunk;
-// each chunk is one workgroup of kScanWaves waves that keeps a top-k.
+// Semantic scan: the scored rows of all sequences, laid end to end, are cut
+// into kScanWaveSlots equal ranges, one per wave (kScanWaves per workgroup).
+// A wave writes one top-k list per sequence its range meets, so a sequence
+// has at most min(kScanWaveSlots, its row count) lists.  The workgroup keeps
+// the row offset, length and candidate count of up to kMaxScanSeqs sequences
+// in LDS.
 constexpr int kScanWaves = 4;
-constexpr int kRowsPerChunk = 64;
+constexpr int kScanWaveSlots = 1024;
+constexpr int kMaxScanSeqs = 2048;
 
-inline int scan_chunks(int L_stride) {
-  int rows = L_stride > 1 ? L_stride - 1 : 1;
-  // a lexical hit scores at most L_stride candidates; the fallback L_stride-1 rows
-  int r = L_stride > rows ? L_stride : rows;
-  return (r + kRowsPerChunk - 1) / kRowsPerChunk;
-}
+inline int scan_lists(int L_stride) { return L_stride < kScanWaveSlots ? L_stride : kScanWaveSlots; }
 
 // Verify attention: keys are processed in tiles of kKeyTile; query rows
 // (node u, head-in-group) are stacked per kv head, 32 rows per MFMA block.

@@ -136,6 +136,27 @@ __device__ __forceinline__ uint64_t bitonic_sort_desc(uint64_t v) {
   return v;
 }
 
+// s_waitcnt vmcnt(n) (gfx9 encoding, n < 64); lgkmcnt and expcnt unconstrained.
+template <int N>
+__device__ __forceinline__ void waitcnt_vm() {
+  __builtin_amdgcn_s_waitcnt(0x0f70 | (N & 15) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
+
+// One wave-wide direct-to-LDS load: lane i's 16 bytes at gptr land at
+// lds_base + 16*i.  Written as inline asm so that the compiler does not treat
+// every later LDS read as possibly aliasing the in-flight load (it would wait
+// for all outstanding loads there); callers wait explicitly with vmcnt.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {

@@ -1,22 +1,26 @@
 // Lexical/semantic backoff (Sec. 3.3) and hidden-state reranking (Sec. 3.4).
 //
-// scan kernel: grid (chunks, B), kScanWaves waves per workgroup.  A sequence
-// with a lexical hit gathers its candidate rows; a sequence without one scans
-// every row [0, L-2] (the fallback).  The decision is read on the device from
-// cand_count, so no host synchronisation sits between the lexical match and
-// this step; chunks past a sequence's row count exit at once.
+// Scored rows.  Sequence b scores nrows_b bank rows: its lexical candidates
+// when it has any (rerank), else every row [0, L-2] (the fallback).  The
+// choice is read on the device from cand_count, so no host synchronisation
+// sits between the lexical match and this step.  The scored rows of all
+// sequences are laid end to end (sequence b starts at P_b, the sum of the
+// earlier nrows) and cut into kScanWaveSlots equal contiguous ranges, one per
+// wave of the scan grid: every wave streams the same number of rows, whatever
+// the mix of fallbacks and hits.
 //
-// Each wave streams bank rows through 16-byte loads (lane l reads elements
-// 8*(l + 64*i) .. +7 of a row), holds the query slice for those elements in
-// registers, accumulates the dot product and the squared norm in fp32 with
-// v_dot2c_f32_bf16 (two bf16 products per instruction) and
-// reduces them with fixed DPP butterflies: identical rows produce bit-identical
-// scores, so exact ties are broken only by position.  A wave keeps its top-k
-// as one key per lane (key = ordered score bits : ~position); the waves of a
-// workgroup merge their lists with a bitonic merge and write one list per
-// chunk.
+// scan kernel: each wave streams its range from HBM into a private LDS ring
+// with direct-to-LDS loads (global_load_lds_dwordx4; up to kScanRingBytes in
+// flight per wave, no register staging), reads each row back with 16-byte LDS
+// reads (lane l holds elements 8*(l + 64*i) .. +7), holds the query slice for
+// those elements in registers, accumulates the dot product and the squared
+// norm in fp32 with v_dot2c_f32_bf16 and reduces them with fixed DPP
+// butterflies: identical rows produce bit-identical scores, so exact ties are
+// broken only by position.  The wave keeps a top-k as one key per lane (key =
+// ordered score bits : ~position) and writes it out at the end of every
+// sequence its range touches (a segment).
 //
-// merge kernel: one workgroup per sequence merges the chunk lists (see the
+// merge kernel: one workgroup per sequence merges its segment lists (see the
 // kernel), applies tau to a fallback, decodes positions and scores and sets
 // the kind.
 #include "adapld_internal.h"
@@ -26,8 +30,11 @@ namespace adapld {
 namespace {
 
 constexpr int kScanThreads = kScanWaves * kWave;
+constexpr int kScanRingBytes = 32768;   // LDS ring per wave
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32x4_t lds_u32x4;
 
 // acc + sum of the 8 products of two 8-element bf16 vectors, fp32 accumulation.
 __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b, float acc) {
@@ -37,9 +44,13 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b, float acc) {
   acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.w), __builtin_bit_cast(bf16x2_t, b.w), acc, false);
   return acc;
 }
-// Rows whose loads are in flight together per wave (more for short rows).
+
+// Rows held by a wave's ring: a row occupies NIT KiB (one KiB per 16-byte
+// load of the whole wave); 2 to 8 rows, at most 32 KiB.
 template <int NIT>
-struct RowsInFlight { static constexpr int value = NIT <= 4 ? 8 : (NIT <= 8 ? 4 : 2); };
+struct RingRows {
+  static constexpr int value = (32 / NIT) < 2 ? 2 : ((32 / NIT) > 8 ? 8 : (32 / NIT));
+};
 
 struct ScanArgs {
   const uint16_t* bank;
@@ -47,8 +58,8 @@ struct ScanArgs {
   const int32_t* lens;
   const int32_t* cand_pos;
   const int32_t* cand_count;
-  int L_stride, d, k, nchunk;
-  uint64_t* ws_keys;  // [B][nchunk][k]
+  int B, L_stride, d, k, lists;   // lists = segment-list slots per sequence
+  uint64_t* ws_keys;              // [B][lists][k]
 };
 
 __device__ __forceinline__ void seq_rows(const ScanArgs& a, int b, int& L, int& cc, int& nrows) {
@@ -57,83 +68,198 @@ __device__ __forceinline__ void seq_rows(const ScanArgs& a, int b, int& L, int& 
   nrows = cc > 0 ? cc : max(L - 1, 0);
 }
 
-template <int NIT>
-__global__ __launch_bounds__(kScanThreads) void semantic_scan_kernel(const ScanArgs a) {
-  __shared__ uint64_t s_keys[kScanWaves][kWave];
-  const int b = blockIdx.y;
-  const int chunk = blockIdx.x;
-  int L, cc, nrows;
-  seq_rows(a, b, L, cc, nrows);
-  const int r0 = chunk * kRowsPerChunk;
-  if (r0 >= nrows) return;
-  const int r1 = min(r0 + kRowsPerChunk, nrows);
-  const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
-  const int d = a.d;
-
-  const uint16_t* __restrict__ qptr =
-      a.query ? a.query + (size_t)b * d : a.bank + ((size_t)b * a.L_stride + (L - 1)) * d;
-  uint4 qv[NIT];
-  float qn = 0.f;
-#pragma unroll
-  for (int it = 0; it < NIT; ++it) {
-    const int e = (it * kWave + lane) * 8;
-    qv[it] = e < d ? *reinterpret_cast<const uint4*>(qptr + e) : make_uint4(0, 0, 0, 0);
-    qn = dot8_bf16(qv[it], qv[it], qn);
-  }
-  qn = wave_sum_dpp(qn);
-  const float qnorm = sqrtf(qn);
-
-  const uint16_t* __restrict__ bank_b = a.bank + (size_t)b * a.L_stride * d;
-  const int32_t* __restrict__ cands = a.cand_pos + (size_t)b * a.L_stride;
-  uint64_t mine = 0;
-  constexpr int kRowsInFlight = RowsInFlight<NIT>::value;
-  for (int i0 = r0 + wave * kRowsInFlight; i0 < r1; i0 += kScanWaves * kRowsInFlight) {
-    int pos[kRowsInFlight];
-    bool ok[kRowsInFlight];
-    uint4 hv[kRowsInFlight][NIT];
-#pragma unroll
-    for (int rr = 0; rr < kRowsInFlight; ++rr) {
-      const int i = i0 + rr;
-      int r = cc > 0 ? (i < r1 ? cands[i] : -1) : i;
-      ok[rr] = i < r1 && r >= 0 && r < L;
-      pos[rr] = r;
-      const uint16_t* __restrict__ row = bank_b + (size_t)(ok[rr] ? r : 0) * d;
-#pragma unroll
-      for (int it = 0; it < NIT; ++it) {
-        const int e = (it * kWave + lane) * 8;
-        hv[rr][it] = (ok[rr] && e < d) ? *reinterpret_cast<const uint4*>(row + e)
-                                       : make_uint4(0, 0, 0, 0);
-      }
-    }
-#pragma unroll
-    for (int rr = 0; rr < kRowsInFlight; ++rr) {
-      float dot = 0.f, nn = 0.f;
-#pragma unroll
-      for (int it = 0; it < NIT; ++it) {
-        dot = dot8_bf16(hv[rr][it], qv[it], dot);
-        nn = dot8_bf16(hv[rr][it], hv[rr][it], nn);
-      }
-      dot = wave_sum_dpp(dot);
-      nn = wave_sum_dpp(nn);
-      if (ok[rr]) {  // wave-uniform
-        const float den = sqrtf(nn) * qnorm;
-        const float s = den > 0.f ? dot / den : 0.f;
-        topk_insert(mine, rank_key(s, pos[rr]), a.k);
-      }
-    }
-  }
-
-  s_keys[wave][lane] = mine;
-  __syncthreads();
-  if (wave == 0) {
-#pragma unroll
-    for (int w = 1; w < kScanWaves; ++w) mine = topk_merge(mine, s_keys[w][lane]);
-    if (lane < a.k) a.ws_keys[((size_t)b * a.nchunk + chunk) * a.k + lane] = mine;
-  }
+// Rows are split over W = min(kScanWaveSlots, total) waves, wave w taking
+// [floor(w total / W), floor((w+1) total / W)): never empty, so the waves that
+// meet one sequence are consecutive and each writes one list.
+__device__ __forceinline__ int scan_waves(int total) { return total < kScanWaveSlots ? total : kScanWaveSlots; }
+__device__ __forceinline__ int wave_of_row(int g, int total) {
+  return (int)((((int64_t)g + 1) * scan_waves(total) - 1) / total);
 }
 
-// Merge kernel.  Every chunk list holds its chunk's k largest keys, sorted.
+// Wait until at most `later` rows issued after the oldest one are still in
+// flight (NIT loads per row).
+template <int NIT, int R>
+__device__ __forceinline__ void wait_rows(int later) {
+  static_assert((R - 1) * NIT < 64, "vmcnt holds 6 bits");
+#define ADAPLD_WAIT_ROWS(n) \
+  if (later == n) { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n * NIT) : "memory"); return; }
+  ADAPLD_WAIT_ROWS(0)
+  if constexpr (R > 1) { ADAPLD_WAIT_ROWS(1) }
+  if constexpr (R > 2) { ADAPLD_WAIT_ROWS(2) }
+  if constexpr (R > 3) { ADAPLD_WAIT_ROWS(3) }
+  if constexpr (R > 4) { ADAPLD_WAIT_ROWS(4) }
+  if constexpr (R > 5) { ADAPLD_WAIT_ROWS(5) }
+  if constexpr (R > 6) { ADAPLD_WAIT_ROWS(6) }
+  if constexpr (R > 7) { ADAPLD_WAIT_ROWS(7) }
+#undef ADAPLD_WAIT_ROWS
+}
+
+template <int NIT>
+__global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const ScanArgs a) {
+  constexpr int R = RingRows<NIT>::value;
+  constexpr int kSlotBytes = NIT * 1024;
+  __shared__ __attribute__((aligned(1024))) uint8_t s_ring[kScanWaves][kScanRingBytes];
+  __shared__ int s_start[kMaxScanSeqs + 1];   // P_b
+  __shared__ int s_len[kMaxScanSeqs];         // clamped L
+  __shared__ int s_cc[kMaxScanSeqs];          // clamped candidate count
+  __shared__ int s_win[kScanWaves][kWave];    // bank rows of the wave's next 64 rows (-1: skip)
+  __shared__ int s_pos[kScanWaves][8];
+  __shared__ int s_red[kScanWaves];
+  static_assert(R * kSlotBytes <= kScanRingBytes, "ring overflow");
+
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid / kWave;
+  const int B = a.B;
+  const int d = a.d;
+
+  // P_b for every sequence: a workgroup-wide exclusive scan of nrows_b.
+  int carry = 0;
+  for (int base = 0; base < B; base += kScanThreads) {
+    const int b = base + tid;
+    int n = 0;
+    if (b < B) {
+      int L, cc;
+      seq_rows(a, b, L, cc, n);
+      s_len[b] = L;
+      s_cc[b] = cc;
+    }
+    int incl = n;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int v = __shfl_up(incl, off, kWave);
+      if (lane >= off) incl += v;
+    }
+    if (lane == kWave - 1) s_red[wave] = incl;
+    __syncthreads();
+    int before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kScanWaves; ++w) {
+      before += w < wave ? s_red[w] : 0;
+      total += s_red[w];
+    }
+    if (b < B) s_start[b] = carry + before + incl - n;
+    carry += total;
+    __syncthreads();
+  }
+  if (tid == 0) s_start[B] = carry;
+  __syncthreads();
+  const int rows_total = carry;
+
+  // This wave's range of global rows; waves are independent from here on.
+  const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * kScanWaves + wave);
+  const int nw = scan_waves(rows_total);
+  if (w >= nw) return;
+  const int g0 = (int)((int64_t)w * rows_total / nw);
+  const int g1 = (int)((int64_t)(w + 1) * rows_total / nw);
+  // Sequence holding g0: the last b with P_b <= g0 (empty sequences share P).
+  auto seq_of = [&](int g) {
+    int lo = 0, hi = B;   // P_lo <= g < P_hi
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_start[mid] <= g) lo = mid; else hi = mid;
+    }
+    return lo;
+  };
+
+  const uint32_t ring = __builtin_amdgcn_readfirstlane(lds_addr(&s_ring[wave][0]));
+  const lds_u32x4* ring_p = (const lds_u32x4*)(&s_ring[wave][0]);
+
+  // Producer: issues the loads of row g into ring slot (g - g0) % R.  The
+  // bank rows of 64 rows at a time are resolved by the lanes together (one
+  // candidate load per lane) into s_win.
+  int pb = seq_of(g0);
+  int p_start = s_start[pb], p_end = s_start[pb + 1];
+  auto fill_window = [&](int gw) {
+    const int gl = gw + lane;
+    int r = -1;
+    if (gl < g1) {
+      const int b = seq_of(gl);
+      const int i = gl - s_start[b];
+      const int rr = s_cc[b] > 0 ? a.cand_pos[(size_t)b * a.L_stride + i] : i;
+      r = rr >= 0 && rr < s_len[b] ? rr : -1;   // rows outside [0, L) are skipped
+    }
+    s_win[wave][lane] = r;
+  };
+  auto issue = [&](int g) {
+    while (g >= p_end) {
+      ++pb;
+      p_start = p_end;
+      p_end = s_start[pb + 1];
+    }
+    if (((g - g0) & (kWave - 1)) == 0) fill_window(g);
+    const int r = s_win[wave][(g - g0) & (kWave - 1)];
+    const int slot = (g - g0) % R;
+    if (lane == 0) s_pos[wave][slot] = r;
+    // A skipped row still loads (row 0 of its sequence) so that every row
+    // counts NIT loads in vmcnt.
+    const uint16_t* row = a.bank + ((size_t)pb * a.L_stride + (r >= 0 ? r : 0)) * d;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the slot's previous row has been read
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int e = (it * kWave + lane) * 8;
+      dma16(row + (e < d ? e : 0), ring + slot * kSlotBytes + it * 1024);
+    }
+  };
+
+  // Consumer state: the current segment's sequence, query slice and list.
+  int cb = -1, c_end = g0, list = 0;
+  uint4 qv[NIT];
+  float qnorm = 0.f;
+  uint64_t mine = 0;
+  auto flush = [&]() {
+    if (cb >= 0 && lane < a.k) a.ws_keys[((size_t)cb * a.lists + list) * a.k + lane] = mine;
+    mine = 0;
+  };
+  auto enter = [&](int g) {
+    flush();
+    cb = seq_of(g);
+    c_end = s_start[cb + 1];
+    list = w - wave_of_row(s_start[cb], rows_total);
+    const int L = s_len[cb];
+    const uint16_t* qptr =
+        a.query ? a.query + (size_t)cb * d : a.bank + ((size_t)cb * a.L_stride + max(L - 1, 0)) * d;
+    float qn = 0.f;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int e = (it * kWave + lane) * 8;
+      qv[it] = e < d ? *reinterpret_cast<const uint4*>(qptr + e) : make_uint4(0, 0, 0, 0);
+      qn = dot8_bf16(qv[it], qv[it], qn);
+    }
+    qnorm = sqrtf(wave_sum_dpp(qn));
+  };
+
+  // The first rows go out before the query is fetched, so the two latencies overlap.
+  int gp = g0;
+  for (; gp < g1 && gp - g0 < R; ++gp) issue(gp);
+  enter(g0);
+  for (int g = g0; g < g1; ++g) {
+    wait_rows<NIT, R>(min(gp - g - 1, R - 1));
+    if (g >= c_end) enter(g);
+    const int slot = (g - g0) % R;
+    const int pos = s_pos[wave][slot];
+    float dot = 0.f, nn = 0.f;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int e = (it * kWave + lane) * 8;
+      const u32x4_t raw = ring_p[(slot * kSlotBytes + it * 1024) / 16 + lane];
+      const uint4 hv = e < d ? make_uint4(raw[0], raw[1], raw[2], raw[3]) : make_uint4(0, 0, 0, 0);
+      dot = dot8_bf16(hv, qv[it], dot);
+      nn = dot8_bf16(hv, hv, nn);
+    }
+    if (gp < g1) issue(gp++);   // refills this slot: its data is in registers
+    dot = wave_sum_dpp(dot);
+    nn = wave_sum_dpp(nn);
+    if (pos >= 0) {  // wave-uniform
+      const float den = sqrtf(nn) * qnorm;
+      const float sc = den > 0.f ? dot / den : 0.f;
+      topk_insert(mine, rank_key(sc, pos), a.k);
+    }
+  }
+  flush();
+}
+
+// Merge kernel.  Every segment list holds its segment's k largest keys, sorted.
 // Only keys >= theta can rank, for any theta that at least k keys reach; two
 // such bounds are combined: the largest k-th entry over the lists (that list
 // alone has k keys above it) and the k-th largest list maximum (found by a
@@ -150,15 +276,41 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
                                                                   int32_t* __restrict__ kind) {
   __shared__ uint64_t s_cand[kMaxCand];
   __shared__ uint64_t s_red[kScanWaves];
+  __shared__ int s_sum[kScanWaves][2];
   __shared__ int s_ncand;
   const int b = blockIdx.x;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
   int L, cc, nrows;
   seq_rows(a, b, L, cc, nrows);
-  const int nvalid = (nrows + kRowsPerChunk - 1) / kRowsPerChunk;
+  // P_b and the total row count locate this sequence's segment lists: one per
+  // scan wave whose range meets rows [P_b, P_b + nrows).
+  int before = 0, total = 0;
+  for (int j = threadIdx.x; j < a.B; j += kScanThreads) {
+    int Lj, ccj, nj;
+    seq_rows(a, j, Lj, ccj, nj);
+    before += j < b ? nj : 0;
+    total += nj;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    before += __shfl_xor(before, off, kWave);
+    total += __shfl_xor(total, off, kWave);
+  }
+  if (lane == 0) {
+    s_sum[wave][0] = before;
+    s_sum[wave][1] = total;
+  }
+  __syncthreads();
+  before = total = 0;
+#pragma unroll
+  for (int w = 0; w < kScanWaves; ++w) {
+    before += s_sum[w][0];
+    total += s_sum[w][1];
+  }
+  const int nvalid = nrows > 0 ? wave_of_row(before + nrows - 1, total) - wave_of_row(before, total) + 1 : 0;
   const int k = a.k;
-  const uint64_t* __restrict__ lists = a.ws_keys + (size_t)b * a.nchunk * k;
+  const uint64_t* __restrict__ lists = a.ws_keys + (size_t)b * a.lists * k;
 
   uint64_t th = 0;
   for (int c = threadIdx.x; c < nvalid; c += kScanThreads) {
@@ -230,8 +382,9 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
 }
 
 template <int NIT>
-void launch_scan(const ScanArgs& a, int B, hipStream_t stream) {
-  hipLaunchKernelGGL(semantic_scan_kernel<NIT>, dim3(a.nchunk, B), dim3(kScanThreads), 0, stream, a);
+void launch_scan(const ScanArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(semantic_scan_kernel<NIT>, dim3(kScanWaveSlots / kScanWaves), dim3(kScanThreads), 0,
+                     stream, a);
 }
 
 }  // namespace
@@ -241,12 +394,12 @@ hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, con
                                 int L_stride, int d, int k, float tau, int32_t* topk_pos,
                                 float* topk_score, int32_t* topk_count, int32_t* kind,
                                 uint64_t* ws_keys, hipStream_t stream) {
-  ScanArgs a{bank, query, lens, cand_pos, cand_count, L_stride, d, k, scan_chunks(L_stride), ws_keys};
+  ScanArgs a{bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, scan_lists(L_stride), ws_keys};
   const int nit = (d + 8 * kWave - 1) / (8 * kWave);
   switch (nit) {
 #define ADAPLD_SCAN_CASE(n) \
   case n:                   \
-    launch_scan<n>(a, B, stream); \
+    launch_scan<n>(a, stream); \
     break;
     ADAPLD_SCAN_CASE(1) ADAPLD_SCAN_CASE(2) ADAPLD_SCAN_CASE(3) ADAPLD_SCAN_CASE(4)
     ADAPLD_SCAN_CASE(5) ADAPLD_SCAN_CASE(6) ADAPLD_SCAN_CASE(7) ADAPLD_SCAN_CASE(8)

@@ -87,27 +87,6 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_ca
 // Physical 16-byte chunk of logical chunk c in key row r is c ^ swz(r).
 __device__ __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
 
-// s_waitcnt vmcnt(n) (gfx9 encoding, n < 64); lgkmcnt and expcnt unconstrained.
-template <int N>
-__device__ __forceinline__ void waitcnt_vm() {
-  __builtin_amdgcn_s_waitcnt(0x0f70 | (N & 15) | ((N >> 4) << 14));
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
-}
-
-// One wave-wide direct-to-LDS load: lane i's 16 bytes at gptr land at
-// lds_base + 16*i.  Written as inline asm so that the compiler does not treat
-// every later LDS read as possibly aliasing the in-flight load (it would wait
-// for all outstanding loads there); the pipeline below waits explicitly.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(gptr), "s"(lds_base)
-               : "memory", "m0");
-}
-
 // Issue this wave's share of one K/V tile: 64/WAVES key rows of K and of V,
 // four rows (1 KiB) per instruction.  Keys past kend re-read key kend-1 (in
 // bounds); their logits are masked.

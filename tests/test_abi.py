@@ -47,9 +47,10 @@ def test_workspace_sizes(lib):
     ws = lib.adapld_workspace_bytes
     assert ws(1, 16, 8192, 4096, 8, 52, 32, 8, 128) == 0          # lexical needs none
     sem = ws(2, 16, 8192, 4096, 8, 0, 0, 0, 0)
-    assert sem == 16 * math.ceil(8192 / 64) * 8 * 8
+    assert sem == 16 * 1024 * 8 * 8                                # one list per scan wave (1024) and sequence
+    assert ws(2, 16, 300, 4096, 8, 0, 0, 0, 0) == 16 * 300 * 8 * 8  # at most one per row
     assert ws(2, 16, 8192, 4096, 65, 0, 0, 0, 0) == 0              # k beyond the limit
-    assert ws(4, 16, 8192, 0, 0, 52, 32, 8, 128) > 0
+    assert ws(4, 16, 8192, 0, 0, 52, 32, 8, 128) > 0               # split context
     assert ws(4, 16, 8192, 0, 0, 52, 32, 7, 128) == 0              # Hq % Hkv != 0
     assert ws(9, 16, 8192, 0, 0, 52, 32, 8, 128) == 0
 
@@ -80,6 +81,8 @@ def test_semantic_validation(lib):
     assert f(*args(d=8200)) == UNSUPPORTED
     assert f(*args(bank=ctypes.c_void_p(0x10008))) == INVALID      # misaligned bf16 rows
     assert f(*args(wsb=16)) == WS_SMALL
+    assert f(*args(B=2049)) == UNSUPPORTED                         # sequence offsets live in LDS
+    assert f(*args(B=2048, L=1 << 20)) == UNSUPPORTED              # B * L_stride beyond int32
 
 
 def test_tree_validation(lib):
