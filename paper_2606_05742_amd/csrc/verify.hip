@@ -10,7 +10,11 @@
 //
 // Memory pipeline.  K and V tiles of 64 keys stream through a 4-stage LDS ring
 // with direct-to-LDS loads (global_load_lds_dwordx4): no VGPR staging, and up
-// to three tiles are in flight.  Each 256-byte key row is stored with its
+// to three tiles are in flight.  The K tiles of all stages fill the first
+// 64 KiB and the V tiles the next 64 KiB, so with the stage known at compile
+// time (the main loop is unrolled over the ring) every fragment address is a
+// per-lane offset plus an instruction immediate; full context tiles are
+// loaded from a scalar base address.  Each 256-byte key row is stored with its
 // 16-byte chunks XOR-swizzled by the row index, which keeps both LDS read
 // patterns below free of bank conflicts.  One barrier per tile both publishes
 // the next tile and frees the stage of the tile before the current one.
@@ -107,6 +111,30 @@ __device__ __forceinline__ void issue_tile(const uint16_t* kb, const uint16_t* v
   }
 }
 
+// One wave-wide direct-to-LDS load with a scalar base: lane i's 16 bytes at
+// gbase + voff land at lds_base + 16*i.
+__device__ __forceinline__ void dma16_s(const void* gbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(gbase), "s"(lds_base)
+               : "memory", "m0");
+}
+
+// The same share of a tile whose 64 keys are all below kend (no clamping):
+// the row addresses are a scalar base plus lane offsets fixed per wave.
+template <int WAVES>
+__device__ __forceinline__ void issue_tile_full(const uint16_t* kb, const uint16_t* vb, int k0, uint32_t lk,
+                                                uint32_t lv, int wave, const uint32_t (&voff)[64 / WAVES / 4]) {
+  constexpr int kRowsPerWave = kKeyTile / WAVES;
+#pragma unroll
+  for (int i = 0; i < kRowsPerWave / 4; ++i) {
+    const int row0 = kRowsPerWave * wave + 4 * i;
+    const size_t key0 = (size_t)(k0 + row0);
+    dma16_s(kb + key0 * kD, voff[i], lk + row0 * kRowBytes);
+    dma16_s(vb + key0 * kD, voff[i], lv + row0 * kRowBytes);
+  }
+}
+
 // Wait for this wave's loads of the current tile, then for every wave's (the
 // barrier).  LPW = loads per wave per tile; `later` tiles issued after the
 // current one may stay in flight.  The asm memory clobber keeps LDS reads from
@@ -127,7 +155,7 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   __shared__ uint64_t s_mask[ADAPLD_MAX_TREE_NODES * kMaskWords];
 
   const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   // Workgroups are dispatched round-robin over the 8 XCDs; the row groups of
   // one (kv head, split) get consecutive slots on the same XCD, so the second
   // reader of a K/V tile finds it in that XCD's L2.
@@ -193,19 +221,37 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   const size_t tree_stride = (size_t)a.Hkv * kD;
   const uint32_t smem_base = lds_addr(smem);
 
+  // The ring keeps the K tiles of the kStages stages in the first 64 KiB of
+  // LDS and the V tiles in the next 64 KiB, so every fragment address below is
+  // a lane offset plus an instruction immediate once the stage is known.
+  constexpr int kVRegion = kStages * kTileBytes;
+  constexpr int kRowsPerWave = kKeyTile / WAVES;
+  uint32_t voff[kRowsPerWave / 4];
+#pragma unroll
+  for (int i = 0; i < kRowsPerWave / 4; ++i) {
+    const int row = kRowsPerWave * wave + 4 * i + (lane >> 4);
+    voff[i] = (lane >> 4) * kRowBytes + (((lane & 15) ^ swz(row)) << 4);
+  }
   auto issue = [&](int t) {
-    const uint32_t lk = smem_base + (t % kStages) * 2 * kTileBytes;
-    if (t < n_ctx)
-      issue_tile<WAVES>(kc, vc, kD, c0 + t * kKeyTile, c1, lk, lk + kTileBytes, wave, lane);
-    else
+    const uint32_t lk = smem_base + (t % kStages) * kTileBytes;
+    const uint32_t lv = lk + kVRegion;
+    if (t < n_ctx) {
+      const int k0 = c0 + t * kKeyTile;
+      if (k0 + kKeyTile <= c1)
+        issue_tile_full<WAVES>(kc, vc, k0, lk, lv, wave, voff);
+      else
+        issue_tile<WAVES>(kc, vc, kD, k0, c1, lk, lv, wave, lane);
+    } else {
       issue_tile<WAVES>(a.k_tree + tree_off, a.v_tree + tree_off, tree_stride, (t - n_ctx) * kKeyTile, T,
-                        lk, lk + kTileBytes, wave, lane);
+                        lk, lv, wave, lane);
+    }
   };
 
   // Lane-dependent LDS byte offsets within a stage.  K fragment for dims
   // [16*ds + 8*half, +8) of key row kb*32 + col sits at kofs[ds] + kb*32*kRowBytes.
   // Transposed V reads: each 16-lane group covers 4 keys x 16 dims; the key rows
-  // are kb*32 + 16*s2 + vkey (+8), whose swizzle depends on vkey only.
+  // are kb*32 + 16*s2 + vkey (+8), whose swizzle depends on vkey only.  vofs
+  // include the offset of the V region.
   int kofs[kD / 16];
 #pragma unroll
   for (int ds = 0; ds < kD / 16; ++ds) kofs[ds] = col * kRowBytes + (((2 * ds + half) ^ swz(col)) << 4);
@@ -215,16 +261,18 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
 #pragma unroll
   for (int db = 0; db < kD / 32; ++db) {
     const int cch = (db * 32 + vdim) >> 3;
-    vofs[0][db] = vkey * kRowBytes + ((cch ^ swz(vkey)) << 4) + (vdim & 7) * 2;
-    vofs[1][db] = (vkey + 8) * kRowBytes + ((cch ^ swz(vkey + 8)) << 4) + (vdim & 7) * 2;
+    vofs[0][db] = kVRegion + vkey * kRowBytes + ((cch ^ swz(vkey)) << 4) + (vdim & 7) * 2;
+    vofs[1][db] = kVRegion + (vkey + 8) * kRowBytes + ((cch ^ swz(vkey + 8)) << 4) + (vdim & 7) * 2;
   }
   const float sl2 = a.scale_log2;
 
   static_assert(NB == 1, "software-pipelined loop handles one 32-row block per wave");
   // Half h covers keys [32*(h&1), +32) of tile h>>1, which sits in stage (h>>1) % kStages.
-  auto stage_of = [&](int h) { return (const lds_u8*)smem + ((h >> 1) & (kStages - 1)) * 2 * kTileBytes; };
+  auto kstage = [&](int h) {
+    return (const lds_u8*)smem + ((h >> 1) & (kStages - 1)) * kTileBytes + (h & 1) * 32 * kRowBytes;
+  };
   auto qk = [&](int h, f32x16_t& sacc) {
-    const lds_u8* kbase = stage_of(h) + (h & 1) * 32 * kRowBytes;
+    const lds_u8* kbase = kstage(h);
     sacc = f32x16_t{};
 #pragma unroll
     for (int ds = 0; ds < kD / 16; ++ds) {
@@ -232,8 +280,34 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[0][ds], sacc, 0, 0, 0);
     }
   };
+  // Fixed-half variants: HS = half index modulo 8.
+  auto qk_c = [&](auto HS, f32x16_t& sacc) {
+    constexpr int hs = decltype(HS)::value;
+    const lds_u8* kbase = (const lds_u8*)smem + ((hs >> 1) & (kStages - 1)) * kTileBytes + (hs & 1) * 32 * kRowBytes;
+    sacc = f32x16_t{};
+#pragma unroll
+    for (int ds = 0; ds < kD / 16; ++ds) {
+      const bf16x8_t ka = *reinterpret_cast<const lds_bf16x8_t*>(kbase + kofs[ds]);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[0][ds], sacc, 0, 0, 0);
+    }
+  };
+  auto pv_c = [&](auto HS, const bf16x8_t (&pbv)[2]) {
+    constexpr int hs = decltype(HS)::value;
+    const lds_u8* vbase = (const lds_u8*)smem + ((hs >> 1) & (kStages - 1)) * kTileBytes + (hs & 1) * 32 * kRowBytes;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db) {
+        const lds_u8* vb2 = vbase + 16 * s2 * kRowBytes;
+        const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vb2 + vofs[0][db]));
+        const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vb2 + vofs[1][db]));
+        const s16x8_t vv = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv), pbv[s2], o[0][db], 0, 0, 0);
+      }
+    }
+  };
   auto pv = [&](int h, const bf16x8_t (&pbv)[2]) {
-    const lds_u8* vbase = stage_of(h) + kTileBytes + (h & 1) * 32 * kRowBytes;
+    const lds_u8* vbase = kstage(h);   // vofs include the V region
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
 #pragma unroll
@@ -333,7 +407,37 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
       exp_pack(s_cur, pb);
       s_cur = s_nxt;
     };
+    // The same step for an unmasked half whose index modulo 8 (two halves per
+    // stage, kStages stages) is the compile-time J: every LDS address is then
+    // a lane offset plus an immediate.
+    auto body_c = [&](auto J, int h) {
+      constexpr int j = decltype(J)::value;
+      pv_c(std::integral_constant<int, (j + 7) & 7>{}, pb);
+      max_rescale(h, s_cur, std::false_type{});
+      if ((j & 1) && h + 1 < H) next_tile(h >> 1);
+      qk_c(std::integral_constant<int, (j + 1) & 7>{}, s_nxt);
+      exp_pack(s_cur, pb);
+      s_cur = s_nxt;
+    };
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    using I4 = std::integral_constant<int, 4>;
+    using I5 = std::integral_constant<int, 5>;
+    using I6 = std::integral_constant<int, 6>;
+    using I7 = std::integral_constant<int, 7>;
+    using I0 = std::integral_constant<int, 0>;
     int h = 1;
+    for (; h + 8 <= H_plain; h += 8) {   // h = 1 (mod 8) here
+      body_c(I1{}, h);
+      body_c(I2{}, h + 1);
+      body_c(I3{}, h + 2);
+      body_c(I4{}, h + 3);
+      body_c(I5{}, h + 4);
+      body_c(I6{}, h + 5);
+      body_c(I7{}, h + 6);
+      body_c(I0{}, h + 7);
+    }
     for (; h < H_plain; ++h) body(h, std::false_type{});
     for (; h < H; ++h) body(h, std::true_type{});
     pv(H - 1, pb);
