@@ -9,7 +9,8 @@
 // each thread over a contiguous run of positions, and compacts
 // {j : len(j) >= n*} in ascending order with a wave scan and a 16-entry
 // workgroup scan of the per-thread hit counts.  A context that fits one piece
-// is staged once.
+// is staged once and scanned once: the match lengths stay in registers
+// between the two steps.
 #include "adapld_internal.h"
 #include "device_utils.h"
 
@@ -62,6 +63,67 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
 
   if (tid < n_max && tid < L) s_suffix[tid] = M[L - 1 - tid];
   const int npieces = J > 0 ? (J + kLexChunk - 1) / kLexChunk : 0;
+
+  // A context that fits one piece is staged once: each thread keeps the match
+  // lengths of its contiguous run of positions in registers (4 bits each), so
+  // n* and the ordered compaction need no second pass over LDS.
+  int found = 0;
+  if (npieces == 1 && n_max <= 15) {
+    const int per = (J + kLexThreads - 1) / kLexThreads;   // <= kLexChunk / kLexThreads = 16
+    const int q0 = tid * per;
+    stage(M, s_tok, 0, 0, J);
+    __syncthreads();
+    uint64_t lens4 = 0;   // 4 bits per position (n_max <= 15 here)
+    int best = 0;
+    for (int e = 0; e < per; ++e) {
+      const int j = q0 + e;
+      if (j < J) {
+        const int n = suffix_len(s_tok, 0, s_suffix, j, min(n_max, j + 1));
+        lens4 |= (uint64_t)n << (4 * e);
+        best = max(best, n);
+      }
+    }
+    best = wave_max_i32(best);
+    if (lane == 0) s_red[wave] = best;
+    __syncthreads();
+    int n_star = 0;
+#pragma unroll
+    for (int w = 0; w < kLexWaves; ++w) n_star = max(n_star, s_red[w]);
+    if (n_star > 0) {
+      uint32_t bits = 0;
+      for (int e = 0; e < per; ++e)
+        if ((int)((lens4 >> (4 * e)) & 15) >= n_star) bits |= 1u << e;
+      const int cnt = __popc(bits);
+      int incl = cnt;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int v = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += v;
+      }
+      __syncthreads();  // the n* reads of s_red are done
+      if (lane == kWave - 1) s_red[wave] = incl;
+      __syncthreads();
+      int before = 0;
+#pragma unroll
+      for (int w = 0; w < kLexWaves; ++w) {
+        const int c = s_red[w];
+        before += (w < wave) ? c : 0;
+        found += c;
+      }
+      int32_t* __restrict__ out = cand_pos + (size_t)b * L_stride;
+      int slot = before + incl - cnt;
+      while (bits) {
+        const int e = __ffs(bits) - 1;
+        bits &= bits - 1;
+        out[slot++] = q0 + e;
+      }
+    }
+    if (tid == 0) {
+      cand_count[b] = found;
+      match_n[b] = n_star;
+    }
+    return;
+  }
 
   // Pass 1: n* = max over j of the capped common-suffix length.
   int best = 0;
