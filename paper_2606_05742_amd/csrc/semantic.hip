@@ -262,8 +262,8 @@ __global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const Sc
 // Merge kernel.  Every segment list holds its segment's k largest keys, sorted.
 // Only keys >= theta can rank, for any theta that at least k keys reach; two
 // such bounds are combined: the largest k-th entry over the lists (that list
-// alone has k keys above it) and the k-th largest list maximum (found by a
-// ballot radix select on the score bits of up to 512 list heads).  The keys
+// alone has k keys above it) and the k-th largest of 64 per-lane maxima of
+// the list heads (a bitonic sort of one register per lane).  The keys
 // that pass are gathered into LDS in one coalesced pass and merged by one
 // wave.  If the gather overflows (adversarial score layouts), the lists are
 // merged one by one instead.
@@ -319,23 +319,16 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
   }
   th = wave_max_u64(th);
   if (wave == 0 && nvalid >= k) {
-    // k-th largest score among the heads of the first 512 lists (8 per lane).
-    uint32_t hs[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int c = lane + kWave * i;
-      hs[i] = c < nvalid ? (uint32_t)(lists[(size_t)c * k] >> 32) : 0u;
+    // Lane l takes the largest head of lists l, l+64, ..., l+448; the k-th
+    // largest of these 64 maxima is reached by at least k heads, so it bounds
+    // the final k-th key from below.
+    uint64_t y = 0;
+    for (int c = lane; c < nvalid && c < 8 * kWave; c += kWave) {
+      const uint64_t h = lists[(size_t)c * k];
+      y = h > y ? h : y;
     }
-    // Greedy MSB-first: the largest x with #{heads >= x} >= k is the k-th largest head.
-    uint32_t prefix = 0;
-    for (int bit = 31; bit >= 0; --bit) {
-      const uint32_t cand = prefix | (1u << bit);
-      int cnt = 0;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) cnt += __popcll(__ballot(hs[i] >= cand));
-      if (cnt >= k) prefix = cand;
-    }
-    const uint64_t thb = (uint64_t)prefix << 32;
+    y = bitonic_sort_desc(y);
+    const uint64_t thb = shfl_u64(y, k - 1);
     th = thb > th ? thb : th;
   }
   if (lane == 0) s_red[wave] = th;
