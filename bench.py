@@ -62,20 +62,37 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(cfg, lens, cand_count, node_count):
-    """Bytes the method must move per step (each input read once, each output written once)."""
+MFMA_PEAK_BF16_TFLOPS = 2500.0
+
+
+def algorithmic_work(cfg, lens, cand_count, node_count, node_depth):
+    """Bytes and flops the method must move and compute per step, per kernel group.
+
+    Each input byte is read once and each output byte written once.  Verify
+    flops count 4*D per (query, key) pair over the context keys and the
+    ancestor-or-self tree keys of every node.
+    """
     d, D, Hq, Hkv = cfg.d, cfg.D, cfg.Hq, cfg.Hkv
-    total = verify = scan = 0
+    lex = scan = ver = ver_flops = 0
     for b in range(len(lens)):
         L = int(lens[b])
         T = int(node_count[b])
         rows = int(cand_count[b]) if int(cand_count[b]) > 0 else max(L - 1, 0)
-        scan_b = 2 * d * rows + 2 * d                                   # scored rows + query
-        ver_b = 4 * Hkv * D * (L + T) + 4 * Hq * D * T + 4 * Hq * T if T > 0 else 0
-        total += 4 * L + scan_b + ver_b
-        scan += scan_b
-        verify += ver_b
-    return total, scan, verify
+        lex += 4 * L
+        scan += 2 * d * rows + 2 * d                                    # scored rows + query
+        if T > 0:
+            ver += 4 * Hkv * D * (L + T) + 4 * Hq * D * T + 4 * Hq * T
+            ver_flops += 4 * Hq * D * sum(L + int(node_depth[b, u]) + 1 for u in range(T))
+    return {"lexical": lex, "semantic": scan, "verify": ver, "verify_flops": ver_flops,
+            "total": lex + scan + ver}
+
+
+def ideal_step_us(work):
+    """t* = sum over kernel groups of max(bytes / HBM peak, flops / bf16 MFMA peak)."""
+    hbm = HBM_PEAK_GBS * 1e3   # bytes per microsecond
+    mfma = MFMA_PEAK_BF16_TFLOPS * 1e6   # flops per microsecond
+    return (work["lexical"] / hbm + work["semantic"] / hbm
+            + max(work["verify"] / hbm, work["verify_flops"] / mfma))
 
 
 def cpu_baseline(cfg, x, min_seconds=10.0):
@@ -114,6 +131,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="one JSON line per workload (the parity configurations), no CPU baseline")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -137,8 +157,17 @@ def main():
     import paper_2606_05742_amd as adapld
     from paper_2606_05742_amd.synth import BENCH_CONFIG, CONFIGS, make_inputs
 
-    name = args.workload or BENCH_CONFIG
-    cfg = CONFIGS[name]
+    names = list(CONFIGS) if args.all_configs else [args.workload or BENCH_CONFIG]
+    for name in names:
+        rec, x, cfg = measure(adapld, CONFIGS[name], name, make_inputs, args)
+        if not args.no_cpu_baseline and not args.all_configs:
+            log("[bench] cpu baseline (oracle)")
+            rec["cpu_baseline"] = cpu_baseline(cfg, x)
+        print(json.dumps(rec), flush=True)
+
+
+def measure(adapld, cfg, name, make_inputs, args):
+    import torch
     log(f"[bench] generating {name}")
     x = make_inputs(cfg)
 
@@ -147,15 +176,19 @@ def main():
 
     tokens = torch.from_numpy(x["tokens"]).cuda()
     lens = torch.from_numpy(x["lens"]).cuda()
+    # Enough input copies that consecutive uses of one copy are more than
+    # 1 GiB of traffic apart (the last-level cache is 256 MB).
+    per_copy = sum(x[k].nbytes for k in ("bank", "q", "k_ctx", "v_ctx", "k_tree", "v_tree"))
+    n_copies = int(min(128, max(2, -(-(1 << 30) // per_copy))))
     sets = []
-    for _ in range(2):
+    for _ in range(n_copies):
         sets.append(dict(bank=up_bf16(x["bank"]), q=up_bf16(x["q"]), k_ctx=up_bf16(x["k_ctx"]),
                          v_ctx=up_bf16(x["v_ctx"]), k_tree=up_bf16(x["k_tree"]), v_tree=up_bf16(x["v_tree"])))
     bufs = adapld.StepBuffers.allocate(cfg.B, cfg.L, cfg.d, cfg.k, cfg.T_max, cfg.Hq, cfg.Hkv, cfg.D)
     stream = torch.cuda.current_stream()
 
     def run(i, ev=None):
-        s = sets[i % 2]
+        s = sets[i % n_copies]
         adapld.lexical_match(tokens, lens, cfg.n_max, cand_pos=bufs.cand_pos, cand_count=bufs.cand_count,
                              match_n=bufs.match_n)
         adapld.semantic_topk(s["bank"], lens, bufs.cand_pos, bufs.cand_count, cfg.k, topk_pos=bufs.topk_pos,
@@ -166,56 +199,93 @@ def main():
                                 node_depth=bufs.node_depth, node_src=bufs.node_src,
                                 node_count=bufs.node_count, tree_mask=bufs.tree_mask)
         if ev is not None:
-            ev[0].record(stream)
+            ev[1].record(stream)
         adapld.tree_verify_attn(s["q"], s["k_ctx"], s["v_ctx"], s["k_tree"], s["v_tree"], lens,
                                 bufs.node_count, bufs.tree_mask, out=bufs.out, lse=bufs.lse, ws=bufs.ws_ver)
         if ev is not None:
-            ev[1].record(stream)
+            ev[2].record(stream)
 
-    log(f"[bench] warmup {args.warmup}")
-    for i in range(args.warmup):
+    steps, warmup = args.steps, args.warmup
+    log(f"[bench] {name}: {n_copies} input copies, warmup {warmup}")
+    for i in range(warmup):
         run(i)
     torch.cuda.synchronize()
     cand_count = bufs.cand_count.cpu().numpy()
     node_count = bufs.node_count.cpu().numpy()
+    node_depth = bufs.node_depth.cpu().numpy()
     kinds = bufs.kind.cpu().numpy()
 
-    log(f"[bench] timing {args.steps} steps")
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    log(f"[bench] timing {steps} steps")
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record(stream)
-    for i in range(args.steps):
+    for i in range(steps):
+        evs[i][0].record(stream)
         run(i, evs[i])
     t_end.record(stream)
     torch.cuda.synchronize()
-    step_ms = t_start.elapsed_time(t_end) / args.steps
-    ver_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    step_ms = t_start.elapsed_time(t_end) / steps
+    per_step_us = np.array([e[0].elapsed_time(e[2]) for e in evs]) * 1e3
+    ver_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     log(f"[bench] step {step_ms * 1e3:.1f} us, verify {ver_ms * 1e3:.1f} us")
 
-    total_b, scan_b, ver_b = algorithmic_bytes(cfg, x["lens"], cand_count, node_count)
+    # The same step captured once per input copy in a HIP graph and replayed.
+    graph_us = None
+    if not args.no_graph:
+        graphs = []
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            for j in range(n_copies):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=side):
+                    run(j)
+                graphs.append(g)
+        stream.wait_stream(side)
+        for i in range(min(warmup, 4)):
+            graphs[i % n_copies].replay()
+        torch.cuda.synchronize()
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for i in range(steps):
+            graphs[i % n_copies].replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        graph_us = g0.elapsed_time(g1) / steps * 1e3
+        del graphs
+
+    work = algorithmic_work(cfg, x["lens"], cand_count, node_count, node_depth)
+    total_b, ver_b = work["total"], work["verify"]
     step_gbs = total_b / (step_ms * 1e-3) / 1e9
     ver_gbs = ver_b / (ver_ms * 1e-3) / 1e9
+    t_star = ideal_step_us(work)
     n_fb = int((cand_count == 0).sum())
     rec = {
         "metric": METRIC,
         "value": cfg.B / (step_ms * 1e-3),
         "unit": "drafts/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": step_ms,
         "step_us": step_ms * 1e3,
+        "step_us_p10_p50_p90": [float(np.percentile(per_step_us, q)) for q in (10, 50, 90)],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": name, "B": cfg.B, "L": cfg.L, "d": cfg.d, "Hq": cfg.Hq, "Hkv": cfg.Hkv,
-                   "D": cfg.D, "n_max": cfg.n_max, "k": cfg.k, "W": cfg.W, "S": cfg.S, "T_max": cfg.T_max},
+                   "D": cfg.D, "n_max": cfg.n_max, "k": cfg.k, "W": cfg.W, "S": cfg.S, "T_max": cfg.T_max,
+                   "input_copies": n_copies},
         "step_hbm": {"algorithmic_bytes": total_b, "achieved_GBs": step_gbs, "peak_GBs": HBM_PEAK_GBS,
                      "frac": step_gbs / HBM_PEAK_GBS},
+        "binding_roofline": {"ideal_step_us": t_star, "frac": t_star / (step_ms * 1e3),
+                             "verify_flops": work["verify_flops"], "mfma_peak_TFLOPs": MFMA_PEAK_BF16_TFLOPS},
+        "graph_step_us": graph_us,
         "draft_nodes_per_s": float(node_count.sum()) / (step_ms * 1e-3),
         "fallback_sequences": n_fb,
         "kinds": {"lex": int((kinds == 1).sum()), "sem": int((kinds == 2).sum()), "none": int((kinds == 0).sum())},
@@ -223,10 +293,11 @@ def main():
                      "unit": "GB/s", "frac": ver_gbs / HBM_PEAK_GBS, "traffic": verify_traffic(name),
                      "algorithmic_bytes_per_launch": ver_b, "launch_us": ver_ms * 1e3},
     }
-    if not args.no_cpu_baseline:
-        log("[bench] cpu baseline (oracle)")
-        rec["cpu_baseline"] = cpu_baseline(cfg, x)
-    print(json.dumps(rec), flush=True)
+    del sets, bufs
+    torch.cuda.empty_cache()
+    return rec, x, cfg
+
+
 
 
 if __name__ == "__main__":

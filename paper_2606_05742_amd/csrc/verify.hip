@@ -491,24 +491,41 @@ __global__ __launch_bounds__(256) void verify_combine_kernel(const VerifyArgs a)
   const int u = qr / a.G;
   const int h = g * a.G + (qr - u * a.G);
   const int dim = (threadIdx.x & 31) * 4;
+  const size_t row0 = (size_t)bg * a.nsplit * a.rows_max + qr;   // split 0 of this row
+  // Loads are issued in groups (8 maxima, then 4 partials) so that many splits
+  // cost a few memory round trips; the splits are summed in index order.
   float M = -INFINITY;
-  for (int s = 0; s < a.nsplit; ++s) {
-    const float2 ml = a.ws_ml[((size_t)bg * a.nsplit + s) * a.rows_max + qr];
-    if (ml.y > 0.f) M = fmaxf(M, ml.x);
+  for (int s0 = 0; s0 < a.nsplit; s0 += 8) {
+    float2 ml[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      ml[j] = s0 + j < a.nsplit ? a.ws_ml[row0 + (size_t)(s0 + j) * a.rows_max] : make_float2(-INFINITY, 0.f);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (ml[j].y > 0.f) M = fmaxf(M, ml[j].x);
   }
   float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
   float den = 0.f;
-  for (int s = 0; s < a.nsplit; ++s) {
-    const size_t slot = ((size_t)bg * a.nsplit + s) * a.rows_max + qr;
-    const float2 ml = a.ws_ml[slot];
-    if (ml.y > 0.f) {
-      const float w = exp2f(ml.x - M);
-      const float4 v = *reinterpret_cast<const float4*>(a.ws_o + slot * kD + dim);
-      num.x += w * v.x;
-      num.y += w * v.y;
-      num.z += w * v.z;
-      num.w += w * v.w;
-      den += w * ml.y;
+  for (int s0 = 0; s0 < a.nsplit; s0 += 4) {
+    float2 ml[4];
+    float4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool in = s0 + j < a.nsplit;
+      const size_t slot = row0 + (size_t)(s0 + j) * a.rows_max;
+      ml[j] = in ? a.ws_ml[slot] : make_float2(-INFINITY, 0.f);
+      v[j] = in ? *reinterpret_cast<const float4*>(a.ws_o + slot * kD + dim) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (ml[j].y > 0.f) {
+        const float w = exp2f(ml[j].x - M);
+        num.x += w * v[j].x;
+        num.y += w * v[j].y;
+        num.z += w * v[j].z;
+        num.w += w * v[j].w;
+        den += w * ml[j].y;
+      }
     }
   }
   const float inv = 1.f / den;
@@ -532,10 +549,12 @@ VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv) {
   p.waves = blocks > 4 ? 8 : 4;
   p.rows_per_wg = p.waves * p.nb * 32;
   p.rowgroups = (p.rows_max + p.rows_per_wg - 1) / p.rows_per_wg;
-  // About one workgroup per CU (256 CUs), splits no shorter than 512 keys.
+  // About one workgroup per CU (256 CUs), splits no shorter than four tiles:
+  // small batches split the context finely, since a workgroup's time is then
+  // mostly the latency of its first tiles.
   const int base = std::max(1, B * Hkv * p.rowgroups);
   const int want = std::max(1, (256 + base - 1) / base);
-  const int max_split = std::max(1, (L_stride + 511) / 512);
+  const int max_split = std::max(1, (L_stride + 4 * kKeyTile - 1) / (4 * kKeyTile));
   p.nsplit = std::min(want, max_split);
   int chunk = (L_stride + p.nsplit - 1) / p.nsplit;
   chunk = ((chunk + kKeyTile - 1) / kKeyTile) * kKeyTile;

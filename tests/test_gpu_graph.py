@@ -1,0 +1,93 @@
+"""The four-call step captured in a HIP graph and replayed.
+
+Every replay must reproduce the eager step bit for bit, also with other eager
+work (a different batch through the same buffers) and host synchronisations
+between the replays.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_05742_amd as adapld
+from paper_2606_05742_amd.synth import make_inputs, small_config
+from parity_helpers import dev_bf16, dev_i32
+
+pytestmark = pytest.mark.gpu
+
+OUTPUTS = ("cand_pos", "cand_count", "match_n", "topk_pos", "topk_score", "topk_count", "kind", "node_token",
+           "node_parent", "node_depth", "node_src", "node_count", "tree_mask", "out", "lse")
+
+
+def _upload(x):
+    return [dev_i32(x["tokens"]), dev_i32(x["lens"]), dev_bf16(x["bank"]), dev_bf16(x["q"]),
+            dev_bf16(x["k_ctx"]), dev_bf16(x["v_ctx"]), dev_bf16(x["k_tree"]), dev_bf16(x["v_tree"])]
+
+
+def _run(cfg, bufs, d):
+    tokens, lens, bank, q, kc, vc, kt, vt = d
+    adapld.lexical_match(tokens, lens, cfg.n_max, cand_pos=bufs.cand_pos, cand_count=bufs.cand_count,
+                         match_n=bufs.match_n)
+    adapld.semantic_topk(bank, lens, bufs.cand_pos, bufs.cand_count, cfg.k, topk_pos=bufs.topk_pos,
+                         topk_score=bufs.topk_score, topk_count=bufs.topk_count, kind=bufs.kind, ws=bufs.ws_sem)
+    adapld.build_draft_tree(tokens, lens, bufs.topk_pos, bufs.topk_count, bufs.kind, cfg.W, cfg.S, cfg.T_max,
+                            node_token=bufs.node_token, node_parent=bufs.node_parent, node_depth=bufs.node_depth,
+                            node_src=bufs.node_src, node_count=bufs.node_count, tree_mask=bufs.tree_mask)
+    adapld.tree_verify_attn(q, kc, vc, kt, vt, lens, bufs.node_count, bufs.tree_mask, out=bufs.out, lse=bufs.lse,
+                            ws=bufs.ws_ver)
+
+
+def _snapshot(bufs):
+    return {n: getattr(bufs, n).clone() for n in OUTPUTS}
+
+
+def _poison(bufs):
+    """Fill every output with a sentinel, so entries a call leaves unwritten compare equal."""
+    for n in OUTPUTS:
+        t = getattr(bufs, n)
+        if t.dtype.is_floating_point:
+            t.fill_(-7.0)
+        else:
+            t.fill_(-7 if t.dtype != torch.uint64 else 0)
+
+
+@pytest.mark.parametrize("L", [700, 3000])
+def test_graph_replay_matches_eager(L):
+    # L = 3000 with B = 2 splits the verify context (the combine kernel runs too).
+    cfg = small_config(B=2, L=L, d=512, Hq=8, Hkv=2, k=8, W=4, S=6, n_max=3, seed=97, forced_every=2)
+    other = small_config(B=2, L=L, d=512, Hq=8, Hkv=2, k=8, W=4, S=6, n_max=3, seed=98, forced_every=2)
+    d = _upload(make_inputs(cfg))
+    d_other = _upload(make_inputs(other))
+    bufs = adapld.StepBuffers.allocate(cfg.B, cfg.L, cfg.d, cfg.k, cfg.T_max, cfg.Hq, cfg.Hkv, cfg.D)
+
+    _poison(bufs)
+    _run(cfg, bufs, d)
+    torch.cuda.synchronize()
+    ref = _snapshot(bufs)
+    _poison(bufs)
+    _run(other, bufs, d_other)
+    torch.cuda.synchronize()
+    ref_other = _snapshot(bufs)
+    assert not torch.equal(ref["out"], ref_other["out"])
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            _run(cfg, bufs, d)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+
+    for rep in range(4):
+        _poison(bufs)
+        graph.replay()
+        torch.cuda.synchronize()
+        got = _snapshot(bufs)
+        for n in OUTPUTS:
+            assert torch.equal(got[n], ref[n]), f"replay {rep}: {n} differs from the eager step"
+        # eager work on another batch through the same buffers between replays
+        _poison(bufs)
+        _run(other, bufs, d_other)
+        torch.cuda.synchronize()
+        for n in ("out", "lse", "node_count"):
+            assert torch.equal(getattr(bufs, n), ref_other[n]), f"eager step after replay {rep}: {n}"
