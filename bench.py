@@ -30,8 +30,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "b09907e4ebf10bf85d031de3940792e3ae68faf2b4401fef6468299d71a2be67",
-    "fetch_kib": 268993.4 + 10961.7,
+    "source_sha256": "2254045586fabea4d2aa5c411e638b58d2fa967dbbf036c480dae9f14e916e74",
+    "fetch_kib": 268985.9 + 10971.6,
     "write_kib": 21547.5 + 5628.0,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
