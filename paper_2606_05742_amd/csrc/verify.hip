@@ -88,8 +88,14 @@ struct VerifyArgs {
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// Physical 16-byte chunk of logical chunk c in key row r is c ^ swz(r).
-__device__ __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
+// Physical 16-byte chunk of logical chunk c in key row r is c ^ swz(r).  LDS
+// has 64 four-byte banks (256 bytes per row of banks).  swz is a bijection on
+// every 16 consecutive rows, so a K fragment read (16 lanes per cycle, one
+// chunk of 16 different rows) touches 16 different chunk positions; and the
+// four consecutive rows that 32 lanes of a transposed V read cover get
+// different values of swz >> 2, so their 64-byte column blocks land in four
+// different quarters of the bank row.  Both reads are free of bank conflicts.
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
 
 // Issue this wave's share of one K/V tile: 64/WAVES key rows of K and of V,
 // four rows (1 KiB) per instruction.  Keys past kend re-read key kend-1 (in
