@@ -37,8 +37,10 @@
 // key (the ragged end of the context and the tree tiles) run the same
 // pipeline with the mask applied.
 //
-// Splits write unnormalised partial outputs with their running max and sum to
-// the workspace; a combine kernel merges them with log-sum-exp weights.
+// Splits write their normalised partial outputs O/l in bf16 (half the bytes of
+// fp32; one more rounding of relative size 2^-9, the size of the final
+// output's own) with the running max and sum in fp32; a combine kernel merges
+// them with log-sum-exp weights.
 #include <algorithm>
 #include <type_traits>
 
@@ -82,8 +84,8 @@ struct VerifyArgs {
   float scale_log2;
   uint16_t* out;
   float* lse;
-  float* ws_o;    // [B*Hkv][nsplit][rows_max][D]  unnormalised partial outputs
-  float2* ws_ml;  // [B*Hkv][nsplit][rows_max]     (running max in log2 units, sum)
+  uint16_t* ws_o;  // [B*Hkv][nsplit][rows_max][D]  partial outputs O/l, bf16
+  float2* ws_ml;   // [B*Hkv][nsplit][rows_max]     (running max in log2 units, sum)
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -472,14 +474,17 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
       if (half == 0 && a.lse) a.lse[((size_t)b * a.Hq + h) * a.T_max + u] = (m_run[nb] + log2f(l_tot)) * kLn2;
     } else {
       const size_t slot = ((size_t)bg * a.nsplit + split) * a.rows_max + qr;
-      float* wp = a.ws_o + slot * kD;
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      uint16_t* wp = a.ws_o + slot * kD;
 #pragma unroll
       for (int db = 0; db < kD / 32; ++db)
 #pragma unroll
         for (int r4 = 0; r4 < 4; ++r4) {
           const int dim = db * 32 + 8 * r4 + 4 * half;
-          *reinterpret_cast<float4*>(wp + dim) =
-              make_float4(o[nb][db][4 * r4 + 0], o[nb][db][4 * r4 + 1], o[nb][db][4 * r4 + 2], o[nb][db][4 * r4 + 3]);
+          uint2 pk;
+          pk.x = f32_to_bf16_bits(o[nb][db][4 * r4 + 0] * inv) | (f32_to_bf16_bits(o[nb][db][4 * r4 + 1] * inv) << 16);
+          pk.y = f32_to_bf16_bits(o[nb][db][4 * r4 + 2] * inv) | (f32_to_bf16_bits(o[nb][db][4 * r4 + 3] * inv) << 16);
+          *reinterpret_cast<uint2*>(wp + dim) = pk;
         }
       if (half == 0) a.ws_ml[slot] = make_float2(m_run[nb], l_tot);
     }
@@ -490,50 +495,47 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
 __global__ __launch_bounds__(256) void verify_combine_kernel(const VerifyArgs a) {
   const int qr = blockIdx.x * 8 + (threadIdx.x >> 5);
   const int bg = blockIdx.y;
+  if (qr >= a.rows_max) return;
+  const int dim = (threadIdx.x & 31) * 4;
+  const size_t row0 = (size_t)bg * a.nsplit * a.rows_max + qr;   // split 0 of this row
+  // One pass over the splits in index order, four at a time.  The maxima and
+  // partials of a group are loaded together, and before node_count is known
+  // (every slot is in bounds), so a call with up to four splits costs one
+  // memory round trip; the running max moves online.  Split s carries O_s/l_s
+  // with weight l_s 2^(m_s - M).
+  float M = -INFINITY, den = 0.f;
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = 0; s0 < a.nsplit; s0 += 4) {
+    float2 ml[4];
+    uint2 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool in = s0 + j < a.nsplit;
+      const size_t slot = row0 + (size_t)(s0 + j) * a.rows_max;
+      ml[j] = in ? a.ws_ml[slot] : make_float2(-INFINITY, 0.f);
+      v[j] = in ? *reinterpret_cast<const uint2*>(a.ws_o + slot * kD + dim) : make_uint2(0u, 0u);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (ml[j].y > 0.f) {
+        const float m_new = fmaxf(M, ml[j].x);
+        const float c = exp2f(M - m_new);   // 0 while nothing has been merged
+        const float w = ml[j].y * exp2f(ml[j].x - m_new);
+        num.x = num.x * c + w * bf16_lo(v[j].x);
+        num.y = num.y * c + w * bf16_hi(v[j].x);
+        num.z = num.z * c + w * bf16_lo(v[j].y);
+        num.w = num.w * c + w * bf16_hi(v[j].y);
+        den = den * c + w;
+        M = m_new;
+      }
+    }
+  }
   const int b = bg / a.Hkv;
   const int g = bg - b * a.Hkv;
   const int T = min(max(a.node_count[b], 0), a.T_max);
   if (qr >= T * a.G) return;
   const int u = qr / a.G;
   const int h = g * a.G + (qr - u * a.G);
-  const int dim = (threadIdx.x & 31) * 4;
-  const size_t row0 = (size_t)bg * a.nsplit * a.rows_max + qr;   // split 0 of this row
-  // Loads are issued in groups (8 maxima, then 4 partials) so that many splits
-  // cost a few memory round trips; the splits are summed in index order.
-  float M = -INFINITY;
-  for (int s0 = 0; s0 < a.nsplit; s0 += 8) {
-    float2 ml[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      ml[j] = s0 + j < a.nsplit ? a.ws_ml[row0 + (size_t)(s0 + j) * a.rows_max] : make_float2(-INFINITY, 0.f);
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (ml[j].y > 0.f) M = fmaxf(M, ml[j].x);
-  }
-  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
-  float den = 0.f;
-  for (int s0 = 0; s0 < a.nsplit; s0 += 4) {
-    float2 ml[4];
-    float4 v[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const bool in = s0 + j < a.nsplit;
-      const size_t slot = row0 + (size_t)(s0 + j) * a.rows_max;
-      ml[j] = in ? a.ws_ml[slot] : make_float2(-INFINITY, 0.f);
-      v[j] = in ? *reinterpret_cast<const float4*>(a.ws_o + slot * kD + dim) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (ml[j].y > 0.f) {
-        const float w = exp2f(ml[j].x - M);
-        num.x += w * v[j].x;
-        num.y += w * v[j].y;
-        num.z += w * v[j].z;
-        num.w += w * v[j].w;
-        den += w * ml[j].y;
-      }
-    }
-  }
   const float inv = 1.f / den;
   uint2 pk;
   pk.x = f32_to_bf16_bits(num.x * inv) | (f32_to_bf16_bits(num.y * inv) << 16);
@@ -572,7 +574,7 @@ VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv) {
 size_t verify_ws_bytes(const VerifyPlan& p, int B, int Hkv) {
   if (p.nsplit <= 1) return 0;
   const size_t slots = (size_t)B * Hkv * p.nsplit * p.rows_max;
-  return slots * kD * sizeof(float) + slots * sizeof(float2);
+  return slots * kD * sizeof(uint16_t) + slots * sizeof(float2);
 }
 
 hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx,
@@ -589,8 +591,8 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
   a.scale_log2 = scale * kLog2e;
   a.out = out; a.lse = lse;
   const size_t slots = (size_t)B * Hkv * p.nsplit * p.rows_max;
-  a.ws_o = static_cast<float*>(ws);
-  a.ws_ml = ws ? reinterpret_cast<float2*>(static_cast<char*>(ws) + slots * kD * sizeof(float)) : nullptr;
+  a.ws_o = static_cast<uint16_t*>(ws);
+  a.ws_ml = ws ? reinterpret_cast<float2*>(static_cast<char*>(ws) + slots * kD * sizeof(uint16_t)) : nullptr;
 
   a.rowgroups = p.rowgroups;
   a.n_kvgroups = B * Hkv * p.nsplit;
