@@ -30,9 +30,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "2254045586fabea4d2aa5c411e638b58d2fa967dbbf036c480dae9f14e916e74",
-    "fetch_kib": 268985.9 + 10971.6,
-    "write_kib": 21547.5 + 5628.0,
+    "source_sha256": "211eda1159ca34ad42302b8847d42d9ad20caeeb8db368a49396b5b0cc3ee865",
+    "fetch_kib": 269001.1 + 7100.6,
+    "write_kib": 10939.5 + 5628.0,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
 }
