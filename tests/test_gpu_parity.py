@@ -105,6 +105,47 @@ def test_step_small(kw):
     log("kinds", kinds)
 
 
+EDGE = {
+    # the paper's own anchor rule: a single-token match (n_max = 1)
+    "nmax1": dict(B=3, L=500, d=256, k=6, W=3, S=5, n_max=1, seed=91),
+    # n_max above 15 takes the two-pass lexical path; long copied spans make n* > 15
+    "nmax20": dict(B=3, L=3000, d=256, k=8, W=4, S=6, n_max=20, seed=92, V=40, copy_frac=0.6, span=(24, 48)),
+    # one-node trees: k = W = 1, S = 0, so verify has one query row per head
+    "single_node": dict(B=4, L=400, d=128, Hq=4, Hkv=2, k=1, W=1, S=0, n_max=3, seed=93, forced_every=2),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_configs(name):
+    cfg = small_config(**EDGE[name])
+    x = make_inputs(cfg)
+    if name == "nmax20":   # the last 30 (17) tokens of sequence 0 (1) repeat an earlier window
+        for b, n in ((0, 30), (1, 17)):
+            L = int(x["lens"][b])
+            x["tokens"][b, L - n:L] = x["tokens"][b, 100:100 + n]
+    g = run_step(cfg, upload(x))
+    check_all(cfg, x, g, ctx=name)
+    if name == "nmax20":
+        assert int(g["match_n"].max()) > 15, g["match_n"]
+    if name == "single_node":
+        assert set(int(t) for t in g["node_count"]) <= {0, 1} and int(g["node_count"].max()) == 1
+
+
+def test_verify_padded_tree_rows():
+    """T_max above W(S+1): the padding rows of q, k_tree and v_tree are ignored."""
+    cfg = small_config(B=3, L=700, d=256, Hq=8, Hkv=2, k=8, W=3, S=4, n_max=3, seed=94, forced_every=2)
+    x = make_inputs(cfg)
+    rng = np.random.default_rng(7)
+    pad = 9
+    for name in ("q", "k_tree", "v_tree"):
+        a = x[name]
+        extra = f32_to_bf16_bits(rng.standard_normal((a.shape[0], pad) + a.shape[2:]).astype(np.float32) * 50.0)
+        x[name] = np.concatenate([a, extra], axis=1)
+    g = run_step(cfg, upload(x))
+    assert g["tree_mask"].shape[1] == cfg.T_max + pad
+    check_all(cfg, x, g, ctx="padded")
+
+
 def test_step_ragged_lengths():
     cfg = small_config(B=8, L=600, d=256, Hq=8, Hkv=2, k=8, W=4, S=6, n_max=3, seed=31)
     lens = [600, 1, 0, 2, 3, 4, 577, 65]
