@@ -76,6 +76,55 @@ __device__ __forceinline__ float key_score(uint64_t key) {
   return __uint_as_float(u);
 }
 
+// Lane i receives lane (i ^ M)'s value, M a power of two below 64, with DPP
+// moves and permlane swaps (ALU ops, no LDS round trip).  Layouts: DPP
+// row_ror:n gives lane i the value of lane (i - n) mod 16 within its row of 16;
+// permlane16_swap(v, v) returns {each row pair's even row, its odd row} and
+// permlane32_swap(v, v) {the low 32 lanes, the high 32 lanes}, both broadcast
+// over the pair.
+template <int M>
+__device__ __forceinline__ uint32_t xor_lanes_u32(uint32_t v) {
+  static_assert(M >= 1 && M <= 32 && (M & (M - 1)) == 0, "power of two below 64");
+  if constexpr (M == 1) {
+    return __builtin_amdgcn_mov_dpp(v, 0xb1, 0xf, 0xf, false);   // quad_perm [1,0,3,2]
+  } else if constexpr (M == 2) {
+    return __builtin_amdgcn_mov_dpp(v, 0x4e, 0xf, 0xf, false);   // quad_perm [2,3,0,1]
+  } else if constexpr (M == 4) {
+    const uint32_t down = __builtin_amdgcn_mov_dpp(v, 0x124, 0xf, 0xf, false);   // row_ror:4, from i - 4
+    const uint32_t up = __builtin_amdgcn_mov_dpp(v, 0x12c, 0xf, 0xf, false);     // row_ror:12, from i + 4
+    return (lane_id() & 4) ? down : up;
+  } else if constexpr (M == 8) {
+    return __builtin_amdgcn_mov_dpp(v, 0x128, 0xf, 0xf, false);  // row_ror:8
+  } else if constexpr (M == 16) {
+    const auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return (lane_id() & 16) ? p[0] : p[1];
+  } else {
+    const auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return (lane_id() & 32) ? p[0] : p[1];
+  }
+}
+template <int M>
+__device__ __forceinline__ uint64_t xor_lanes_u64(uint64_t v) {
+  const uint32_t lo = xor_lanes_u32<M>((uint32_t)v);
+  const uint32_t hi = xor_lanes_u32<M>((uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+// Lane i receives lane 63 - i's value.
+__device__ __forceinline__ uint64_t reverse_lanes_u64(uint64_t v) {
+  const uint32_t lo = __builtin_amdgcn_mov_dpp((uint32_t)v, 0x140, 0xf, 0xf, false);          // row_mirror
+  const uint32_t hi = __builtin_amdgcn_mov_dpp((uint32_t)(v >> 32), 0x140, 0xf, 0xf, false);
+  return xor_lanes_u64<32>(xor_lanes_u64<16>(((uint64_t)hi << 32) | lo));
+}
+
+// Lane `src`'s value (uniform src) through the scalar unit.  The builtin
+// returns int: each half is cast to uint32_t before widening, so the low half
+// does not sign-extend into the high one.
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int src) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((uint32_t)v, src);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((uint32_t)(v >> 32), src);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
   uint32_t lo = __shfl((uint32_t)v, src, kWave);
   uint32_t hi = __shfl((uint32_t)(v >> 32), src, kWave);
@@ -96,7 +145,7 @@ __device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int d) {
 // Insert one key that every lane holds (uniform control flow).
 __device__ __forceinline__ void topk_insert(uint64_t& mine, uint64_t key, int k) {
   const int lane = lane_id();
-  const uint64_t last = shfl_u64(mine, k - 1);
+  const uint64_t last = readlane_u64(mine, k - 1);
   if (key <= last) return;                         // uniform: key is wave-uniform
   const uint64_t above = __ballot(lane < k && mine > key);
   const int p = __popcll(above);                   // insertion slot
@@ -108,33 +157,32 @@ __device__ __forceinline__ void topk_insert(uint64_t& mine, uint64_t key, int k)
 // Merge two wave-wide lists sorted descending (64 slots each, empty = 0):
 // the result holds the 64 largest of both, sorted descending.  The elementwise
 // max against the reversed partner list is bitonic; half-cleaners sort it.
+// Half-cleaner steps of distance S, S/2, ..., 1 (descending).
+template <int S>
+__device__ __forceinline__ uint64_t half_clean_desc(uint64_t c) {
+  const uint64_t p = xor_lanes_u64<S>(c);
+  c = (lane_id() & S) == 0 ? (c > p ? c : p) : (c < p ? c : p);
+  if constexpr (S > 1) return half_clean_desc<S / 2>(c);
+  else return c;
+}
 __device__ __forceinline__ uint64_t topk_merge(uint64_t mine, uint64_t other) {
-  const int lane = lane_id();
-  uint64_t rev = shfl_u64(other, 63 - lane);
-  uint64_t c = mine > rev ? mine : rev;
-#pragma unroll
-  for (int s = 32; s >= 1; s >>= 1) {
-    uint64_t p = shfl_xor_u64(c, s);
-    const bool low = (lane & s) == 0;
-    c = low ? (c > p ? c : p) : (c < p ? c : p);
-  }
-  return c;
+  const uint64_t rev = reverse_lanes_u64(other);
+  return half_clean_desc<32>(mine > rev ? mine : rev);
 }
 
-// Sort a wave-wide list of 64 keys descending (bitonic network).
-__device__ __forceinline__ uint64_t bitonic_sort_desc(uint64_t v) {
+// Sort a wave-wide list of 64 keys descending (bitonic network): stage K
+// merges blocks of K, step J compares lanes J apart.
+template <int K, int J>
+__device__ __forceinline__ uint64_t bitonic_steps(uint64_t v) {
   const int lane = lane_id();
-#pragma unroll
-  for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const uint64_t p = shfl_xor_u64(v, j);
-      const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
-      v = keep_max ? (v > p ? v : p) : (v < p ? v : p);
-    }
-  }
-  return v;
+  const uint64_t p = xor_lanes_u64<J>(v);
+  const bool keep_max = ((lane & J) == 0) == ((lane & K) == 0);
+  v = keep_max ? (v > p ? v : p) : (v < p ? v : p);
+  if constexpr (J > 1) return bitonic_steps<K, J / 2>(v);
+  else if constexpr (K < kWave) return bitonic_steps<2 * K, K>(v);
+  else return v;
 }
+__device__ __forceinline__ uint64_t bitonic_sort_desc(uint64_t v) { return bitonic_steps<2, 1>(v); }
 
 // s_waitcnt vmcnt(n) (gfx9 encoding, n < 64); lgkmcnt and expcnt unconstrained.
 template <int N>
@@ -157,13 +205,13 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
                : "memory", "m0");
 }
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint64_t p = shfl_xor_u64(v, off);
-    v = v > p ? v : p;
-  }
-  return v;
+template <int S>
+__device__ __forceinline__ uint64_t wave_max_steps(uint64_t v) {
+  const uint64_t p = xor_lanes_u64<S>(v);
+  v = v > p ? v : p;
+  if constexpr (S > 1) return wave_max_steps<S / 2>(v);
+  else return v;
 }
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) { return wave_max_steps<32>(v); }
 
 }  // namespace adapld

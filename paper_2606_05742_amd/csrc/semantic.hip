@@ -328,7 +328,7 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
       y = h > y ? h : y;
     }
     y = bitonic_sort_desc(y);
-    const uint64_t thb = shfl_u64(y, k - 1);
+    const uint64_t thb = readlane_u64(y, k - 1);
     th = thb > th ? thb : th;
   }
   if (lane == 0) s_red[wave] = th;
