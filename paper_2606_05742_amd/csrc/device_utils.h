@@ -16,10 +16,43 @@ __device__ __forceinline__ uint64_t lanes_below() {
   return l == 0 ? 0ull : (~0ull >> (64 - l));
 }
 
-__device__ __forceinline__ int wave_max_i32(int v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, kWave));
-  return v;
+template <int M> __device__ __forceinline__ uint32_t xor_lanes_u32(uint32_t v);
+
+template <int S>
+__device__ __forceinline__ int wave_max_i32_steps(int v) {
+  v = max(v, (int)xor_lanes_u32<S>((uint32_t)v));
+  if constexpr (S > 1) return wave_max_i32_steps<S / 2>(v);
+  else return v;
+}
+// Max over the wave on DPP moves and permlane swaps; every lane returns it.
+__device__ __forceinline__ int wave_max_i32(int v) { return wave_max_i32_steps<32>(v); }
+
+template <int S>
+__device__ __forceinline__ int wave_sum_i32_steps(int v) {
+  v += (int)xor_lanes_u32<S>((uint32_t)v);
+  if constexpr (S > 1) return wave_sum_i32_steps<S / 2>(v);
+  else return v;
+}
+// Sum over the wave on DPP moves and permlane swaps; every lane returns it.
+__device__ __forceinline__ int wave_sum_i32(int v) { return wave_sum_i32_steps<32>(v); }
+
+// Inclusive prefix sum over the 64 lanes without LDS traffic: DPP row shifts
+// by 1, 2, 4, 8 (lanes shifted in from outside the row of 16 read 0) give the
+// sum within each row; the three lower rows' totals come in as scalars.
+template <int CTRL>
+__device__ __forceinline__ int dpp_shift_in_zero(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
+}
+__device__ __forceinline__ int wave_incl_scan_i32(int v) {
+  v += dpp_shift_in_zero<0x111>(v);   // row_shr:1
+  v += dpp_shift_in_zero<0x112>(v);   // row_shr:2
+  v += dpp_shift_in_zero<0x114>(v);   // row_shr:4
+  v += dpp_shift_in_zero<0x118>(v);   // row_shr:8
+  const int t0 = __builtin_amdgcn_readlane(v, 15);
+  const int t1 = __builtin_amdgcn_readlane(v, 31);
+  const int t2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane_id() >> 4;
+  return v + (row >= 1 ? t0 : 0) + (row >= 2 ? t1 : 0) + (row >= 3 ? t2 : 0);
 }
 
 // Butterfly sum: every lane ends with the same value, and the order of the

@@ -94,12 +94,7 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
       for (int e = 0; e < per; ++e)
         if ((int)((lens4 >> (4 * e)) & 15) >= n_star) bits |= 1u << e;
       const int cnt = __popc(bits);
-      int incl = cnt;
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int v = __shfl_up(incl, off, kWave);
-        if (lane >= off) incl += v;
-      }
+      const int incl = wave_incl_scan_i32(cnt);
       __syncthreads();  // the n* reads of s_red are done
       if (lane == kWave - 1) s_red[wave] = incl;
       __syncthreads();
@@ -165,12 +160,7 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
         if (j < p1 && j >= n_star - 1 && suffix_len(s_tok, p0, s_suffix, j, n_star) == n_star) bits |= 1u << e;
       }
       const int cnt = __popc(bits);
-      int incl = cnt;
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int v = __shfl_up(incl, off, kWave);
-        if (lane >= off) incl += v;
-      }
+      const int incl = wave_incl_scan_i32(cnt);
       __syncthreads();  // earlier reads of s_red are done
       if (lane == kWave - 1) s_red[wave] = incl;
       __syncthreads();

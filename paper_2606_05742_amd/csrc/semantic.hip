@@ -124,12 +124,7 @@ __global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const Sc
       s_len[b] = L;
       s_cc[b] = cc;
     }
-    int incl = n;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-      const int v = __shfl_up(incl, off, kWave);
-      if (lane >= off) incl += v;
-    }
+    const int incl = wave_incl_scan_i32(n);
     if (lane == kWave - 1) s_red[wave] = incl;
     __syncthreads();
     int before = 0, total = 0;
@@ -292,11 +287,8 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
     before += j < b ? nj : 0;
     total += nj;
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    before += __shfl_xor(before, off, kWave);
-    total += __shfl_xor(total, off, kWave);
-  }
+  before = wave_sum_i32(before);
+  total = wave_sum_i32(total);
   if (lane == 0) {
     s_sum[wave][0] = before;
     s_sum[wave][1] = total;

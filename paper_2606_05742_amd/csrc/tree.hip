@@ -38,9 +38,9 @@ __global__ __launch_bounds__(kWave) void build_draft_tree_kernel(
   if (valid) tok = M[r + 1];
   // A lane is a new branch if no lower valid lane holds the same successor token.
   bool dup = false;
-  for (int j = 0; j < cnt; ++j) {
-    const int tj = __shfl(tok, j, kWave);
-    const int vj = __shfl((int)valid, j, kWave);
+  for (int j = 0; j < cnt; ++j) {   // lane j's token and validity as scalars
+    const int tj = __builtin_amdgcn_readlane(tok, j);
+    const int vj = __builtin_amdgcn_readlane((int)valid, j);
     dup |= (j < lane) && vj && tj == tok;
   }
   const bool opens = valid && !dup;
@@ -49,14 +49,9 @@ __global__ __launch_bounds__(kWave) void build_draft_tree_kernel(
   const int len = keep ? min(S + 1, L - 1 - r) : 0;
 
   // Exclusive prefix sum of branch lengths over lanes (branch order = lane order).
-  int incl = len;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int v = __shfl_up(incl, off, kWave);
-    if (lane >= off) incl += v;
-  }
+  const int incl = wave_incl_scan_i32(len);
   const int start = incl - len;
-  const int T = __shfl(incl, kWave - 1, kWave);
+  const int T = __builtin_amdgcn_readlane(incl, kWave - 1);
 
   const size_t nb = (size_t)b * T_max;
   for (int dd = 0; dd < len; ++dd) {
