@@ -20,7 +20,7 @@ namespace {
 constexpr int kLexThreads = 1024;
 constexpr int kLexWaves = kLexThreads / kWave;
 constexpr int kMaxNmax = ADAPLD_MAX_NMAX;
-constexpr int kLexChunk = 16384;   // tokens per LDS piece (64 KiB)
+constexpr int kLexChunk = 32768;   // tokens per LDS piece (128 KiB)
 constexpr int kHalo = kMaxNmax;    // >= n_max - 1, multiple of 4
 
 // Stage tokens [lo, hi) at s_tok[kHalo - (p0 - lo) ...]: s_tok[kHalo + i] holds M[p0 + i].
@@ -69,17 +69,17 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
   // n* and the ordered compaction need no second pass over LDS.
   int found = 0;
   if (npieces == 1 && n_max <= 15) {
-    const int per = (J + kLexThreads - 1) / kLexThreads;   // <= kLexChunk / kLexThreads = 16
+    const int per = (J + kLexThreads - 1) / kLexThreads;   // <= kLexChunk / kLexThreads = 32
     const int q0 = tid * per;
     stage(M, s_tok, 0, 0, J);
     __syncthreads();
-    uint64_t lens4 = 0;   // 4 bits per position (n_max <= 15 here)
+    uint64_t lens4[2] = {0, 0};   // 4 bits per position (n_max <= 15 here), 16 positions per word
     int best = 0;
     for (int e = 0; e < per; ++e) {
       const int j = q0 + e;
       if (j < J) {
         const int n = suffix_len(s_tok, 0, s_suffix, j, min(n_max, j + 1));
-        lens4 |= (uint64_t)n << (4 * e);
+        lens4[e >> 4] |= (uint64_t)n << (4 * (e & 15));
         best = max(best, n);
       }
     }
@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
     if (n_star > 0) {
       uint32_t bits = 0;
       for (int e = 0; e < per; ++e)
-        if ((int)((lens4 >> (4 * e)) & 15) >= n_star) bits |= 1u << e;
+        if ((int)((lens4[e >> 4] >> (4 * (e & 15))) & 15) >= n_star) bits |= 1u << e;
       const int cnt = __popc(bits);
       const int incl = wave_incl_scan_i32(cnt);
       __syncthreads();  // the n* reads of s_red are done

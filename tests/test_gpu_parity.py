@@ -131,6 +131,27 @@ def test_edge_configs(name):
         assert set(int(t) for t in g["node_count"]) <= {0, 1} and int(g["node_count"].max()) == 1
 
 
+@pytest.mark.parametrize("n_max", [6, 20])
+def test_lexical_long_contexts(n_max):
+    """Contexts longer than one LDS piece (32768 tokens): the lexical kernel
+    stages the context piece by piece, with a halo of n_max - 1 tokens."""
+    cfg = small_config(B=3, L=70000, d=8, n_max=n_max, seed=95, V=60, copy_frac=0.5, span=(8, 64))
+    x = make_inputs(cfg, with_bank=False, with_verify=False)
+    L0 = int(x["lens"][0])
+    x["tokens"][0, L0 - 40:L0] = x["tokens"][0, 50000:50040]   # a long suffix repeat in the second piece
+    x["tokens"][2, 32760:32800] = x["tokens"][2, -40:]         # ... and one straddling the piece boundary
+    lens = dev_i32(x["lens"])
+    cp, cc, mn = adapld.lexical_match(dev_i32(x["tokens"]), lens, n_max)
+    torch.cuda.synchronize()
+    cp, cc, mn = cp.cpu().numpy(), cc.cpu().numpy(), mn.cpu().numpy()
+    for b in range(cfg.B):
+        L = int(x["lens"][b])
+        n, C = oracle.lexical_match(x["tokens"][b, :L], n_max)
+        assert int(mn[b]) == n and int(cc[b]) == len(C), (b, int(mn[b]), n, int(cc[b]), len(C))
+        np.testing.assert_array_equal(cp[b, :len(C)], C)
+    assert int(mn[0]) == min(n_max, 40) and int(mn[2]) == min(n_max, 40)
+
+
 def test_verify_padded_tree_rows():
     """T_max above W(S+1): the padding rows of q, k_tree and v_tree are ignored."""
     cfg = small_config(B=3, L=700, d=256, Hq=8, Hkv=2, k=8, W=3, S=4, n_max=3, seed=94, forced_every=2)
