@@ -45,11 +45,99 @@ __device__ __forceinline__ int suffix_len(const int* s_tok, int p0, const int* s
   return n;
 }
 
+// Single pass over a context staged whole in LDS (J = L - 1 <= kLexChunk,
+// n_max <= NM <= 16, per <= PMAX).  Thread tid owns positions
+// [tid * per, +per); per is odd, so the 64 lanes of a wave, reading word
+// tid * per + i at the same time, touch 64 different LDS banks.
+//
+// The match lengths need no data-dependent loop: the run's tokens and the
+// NM - 1 before it are read from LDS into registers once, and the length at j
+// is the number of trailing ones of the mask of k < NM with
+// M[j - k] == M[L - 1 - k], capped at min(n_max, j + 1) (so tokens before
+// position 0, and suffix entries past the cap, never count).  They stay in
+// registers (4 bits each) for the ordered compaction after the workgroup
+// reduction of n*.  NM and PMAX are compile-time bounds, so every register
+// index is a constant.
+template <int NM, int PMAX>
+__device__ __forceinline__ void single_pass(const int* s_tok, const int* s_suffix, int* s_red, int J, int per,
+                                            int n_max, int32_t* __restrict__ out, int32_t* __restrict__ cand_count,
+                                            int32_t* __restrict__ match_n) {
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid / kWave;
+  const int q0 = tid * per;
+  int suf[NM];
+#pragma unroll
+  for (int k = 0; k < NM; ++k) suf[k] = k < n_max ? s_suffix[k] : 0;
+  int w[NM - 1 + PMAX];   // w[i] = M[q0 - (NM - 1) + i]
+#pragma unroll
+  for (int i = 0; i < NM - 1 + PMAX; ++i) w[i] = i < NM - 1 + per ? s_tok[kHalo + q0 - (NM - 1) + i] : 0;
+  uint64_t lens4[(PMAX + 15) / 16] = {};
+  int best = 0;
+#pragma unroll
+  for (int e = 0; e < PMAX; ++e) {
+    const int j = q0 + e;
+    if (e < per && j < J) {
+      uint32_t eq = 0;
+#pragma unroll
+      for (int k = 0; k < NM; ++k) eq |= (uint32_t)(w[e + NM - 1 - k] == suf[k]) << k;
+      const int n = min(__builtin_ctz(~eq), min(n_max, j + 1));
+      lens4[e >> 4] |= (uint64_t)n << (4 * (e & 15));
+      best = max(best, n);
+    }
+  }
+  best = wave_max_i32(best);
+  if (lane == 0) s_red[wave] = best;
+  __syncthreads();
+  int n_star = 0;
+#pragma unroll
+  for (int v = 0; v < kLexWaves; ++v) n_star = max(n_star, s_red[v]);
+  int found = 0;
+  if (n_star > 0) {
+    uint64_t bits = 0;
+#pragma unroll
+    for (int e = 0; e < PMAX; ++e)
+      if (e < per && (int)((lens4[e >> 4] >> (4 * (e & 15))) & 15) >= n_star) bits |= 1ull << e;
+    const int cnt = __popcll(bits);
+    const int incl = wave_incl_scan_i32(cnt);
+    __syncthreads();  // the n* reads of s_red are done
+    if (lane == kWave - 1) s_red[wave] = incl;
+    __syncthreads();
+    int before = 0;
+#pragma unroll
+    for (int v = 0; v < kLexWaves; ++v) {
+      const int c = s_red[v];
+      before += (v < wave) ? c : 0;
+      found += c;
+    }
+    int slot = before + incl - cnt;
+    while (bits) {
+      const int e = __builtin_ctzll(bits);
+      bits &= bits - 1;
+      out[slot++] = q0 + e;
+    }
+  }
+  if (tid == 0) {
+    *cand_count = found;
+    *match_n = n_star;
+  }
+}
+
+template <int NM>
+__device__ __forceinline__ void single_pass_nm(const int* s_tok, const int* s_suffix, int* s_red, int J, int n_max,
+                                               int32_t* out, int32_t* cand_count, int32_t* match_n) {
+  const int per = J > 0 ? ((J + kLexThreads - 1) / kLexThreads) | 1 : 0;   // odd, <= 33
+  if (per <= 9) single_pass<NM, 9>(s_tok, s_suffix, s_red, J, per, n_max, out, cand_count, match_n);
+  else if (per <= 17) single_pass<NM, 17>(s_tok, s_suffix, s_red, J, per, n_max, out, cand_count, match_n);
+  else single_pass<NM, kLexChunk / kLexThreads + 1>(s_tok, s_suffix, s_red, J, per, n_max, out, cand_count, match_n);
+}
+
 __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
     const int32_t* __restrict__ tokens, const int32_t* __restrict__ lens, int L_stride, int n_max,
     int32_t* __restrict__ cand_pos, int32_t* __restrict__ cand_count,
     int32_t* __restrict__ match_n) {
-  __shared__ __attribute__((aligned(16))) int s_tok[kHalo + kLexChunk];
+  // kLexThreads more than one piece: the single pass may round its runs up
+  __shared__ __attribute__((aligned(16))) int s_tok[kHalo + kLexChunk + kLexThreads];
   __shared__ int s_suffix[kMaxNmax];
   __shared__ int s_red[kLexWaves];
 
@@ -64,59 +152,14 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
   if (tid < n_max && tid < L) s_suffix[tid] = M[L - 1 - tid];
   const int npieces = J > 0 ? (J + kLexChunk - 1) / kLexChunk : 0;
 
-  // A context that fits one piece is staged once: each thread keeps the match
-  // lengths of its contiguous run of positions in registers (4 bits each), so
-  // n* and the ordered compaction need no second pass over LDS.
-  int found = 0;
+  // A context that fits one piece is staged once and scanned once.
   if (npieces == 1 && n_max <= 15) {
-    const int per = (J + kLexThreads - 1) / kLexThreads;   // <= kLexChunk / kLexThreads = 32
-    const int q0 = tid * per;
     stage(M, s_tok, 0, 0, J);
     __syncthreads();
-    uint64_t lens4[2] = {0, 0};   // 4 bits per position (n_max <= 15 here), 16 positions per word
-    int best = 0;
-    for (int e = 0; e < per; ++e) {
-      const int j = q0 + e;
-      if (j < J) {
-        const int n = suffix_len(s_tok, 0, s_suffix, j, min(n_max, j + 1));
-        lens4[e >> 4] |= (uint64_t)n << (4 * (e & 15));
-        best = max(best, n);
-      }
-    }
-    best = wave_max_i32(best);
-    if (lane == 0) s_red[wave] = best;
-    __syncthreads();
-    int n_star = 0;
-#pragma unroll
-    for (int w = 0; w < kLexWaves; ++w) n_star = max(n_star, s_red[w]);
-    if (n_star > 0) {
-      uint32_t bits = 0;
-      for (int e = 0; e < per; ++e)
-        if ((int)((lens4[e >> 4] >> (4 * (e & 15))) & 15) >= n_star) bits |= 1u << e;
-      const int cnt = __popc(bits);
-      const int incl = wave_incl_scan_i32(cnt);
-      __syncthreads();  // the n* reads of s_red are done
-      if (lane == kWave - 1) s_red[wave] = incl;
-      __syncthreads();
-      int before = 0;
-#pragma unroll
-      for (int w = 0; w < kLexWaves; ++w) {
-        const int c = s_red[w];
-        before += (w < wave) ? c : 0;
-        found += c;
-      }
-      int32_t* __restrict__ out = cand_pos + (size_t)b * L_stride;
-      int slot = before + incl - cnt;
-      while (bits) {
-        const int e = __ffs(bits) - 1;
-        bits &= bits - 1;
-        out[slot++] = q0 + e;
-      }
-    }
-    if (tid == 0) {
-      cand_count[b] = found;
-      match_n[b] = n_star;
-    }
+    int32_t* __restrict__ out = cand_pos + (size_t)b * L_stride;
+    if (n_max <= 4) single_pass_nm<4>(s_tok, s_suffix, s_red, J, n_max, out, cand_count + b, match_n + b);
+    else if (n_max <= 8) single_pass_nm<8>(s_tok, s_suffix, s_red, J, n_max, out, cand_count + b, match_n + b);
+    else single_pass_nm<16>(s_tok, s_suffix, s_red, J, n_max, out, cand_count + b, match_n + b);
     return;
   }
 

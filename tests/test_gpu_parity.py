@@ -110,6 +110,8 @@ EDGE = {
     "nmax1": dict(B=3, L=500, d=256, k=6, W=3, S=5, n_max=1, seed=91),
     # n_max above 15 takes the two-pass lexical path; long copied spans make n* > 15
     "nmax20": dict(B=3, L=3000, d=256, k=8, W=4, S=6, n_max=20, seed=92, V=40, copy_frac=0.6, span=(24, 48)),
+    # n_max = 12: the single-pass lexical path at its widest match-length template
+    "nmax12": dict(B=3, L=2500, d=256, k=8, W=4, S=6, n_max=12, seed=96, V=40, copy_frac=0.6, span=(24, 48)),
     # one-node trees: k = W = 1, S = 0, so verify has one query row per head
     "single_node": dict(B=4, L=400, d=128, Hq=4, Hkv=2, k=1, W=1, S=0, n_max=3, seed=93, forced_every=2),
 }
@@ -119,7 +121,7 @@ EDGE = {
 def test_edge_configs(name):
     cfg = small_config(**EDGE[name])
     x = make_inputs(cfg)
-    if name == "nmax20":   # the last 30 (17) tokens of sequence 0 (1) repeat an earlier window
+    if name in ("nmax20", "nmax12"):   # the last 30 (17) tokens of sequence 0 (1) repeat an earlier window
         for b, n in ((0, 30), (1, 17)):
             L = int(x["lens"][b])
             x["tokens"][b, L - n:L] = x["tokens"][b, 100:100 + n]
@@ -127,6 +129,8 @@ def test_edge_configs(name):
     check_all(cfg, x, g, ctx=name)
     if name == "nmax20":
         assert int(g["match_n"].max()) > 15, g["match_n"]
+    if name == "nmax12":
+        assert int(g["match_n"].max()) == 12, g["match_n"]
     if name == "single_node":
         assert set(int(t) for t in g["node_count"]) <= {0, 1} and int(g["node_count"].max()) == 1
 
@@ -150,6 +154,29 @@ def test_lexical_long_contexts(n_max):
         assert int(mn[b]) == n and int(cc[b]) == len(C), (b, int(mn[b]), n, int(cc[b]), len(C))
         np.testing.assert_array_equal(cp[b, :len(C)], C)
     assert int(mn[0]) == min(n_max, 40) and int(mn[2]) == min(n_max, 40)
+
+
+@pytest.mark.parametrize("L,n_max", [(9217, 4), (9300, 7), (17500, 13), (32769, 4), (32769, 15)])
+def test_lexical_single_piece_runs(L, n_max):
+    """Contexts of one LDS piece at the edges of the single pass's run-length
+    bounds (9, 17 and 33 positions per thread) and of its n-gram bounds
+    (4, 8 and 16), with ragged lengths and a planted full-length repeat."""
+    cfg = small_config(B=3, L=L, d=8, n_max=n_max, seed=93, V=50, copy_frac=0.5, span=(8, 64))
+    x = make_inputs(cfg, with_bank=False, with_verify=False)
+    x["lens"][:] = [L, L - 513, L // 2 + 7]
+    t = x["tokens"]
+    t[0, L - 20:L] = t[0, 1000:1020]            # n* = n_max in row 0
+    t[1, 16:36] = t[1, L - 513 - 20:L - 513]    # a repeat ending at position 35, near the start
+    lens = dev_i32(x["lens"])
+    cp, cc, mn = adapld.lexical_match(dev_i32(t), lens, n_max)
+    torch.cuda.synchronize()
+    cp, cc, mn = cp.cpu().numpy(), cc.cpu().numpy(), mn.cpu().numpy()
+    for b in range(cfg.B):
+        Lb = int(x["lens"][b])
+        n, C = oracle.lexical_match(t[b, :Lb], n_max)
+        assert int(mn[b]) == n and int(cc[b]) == len(C), (b, int(mn[b]), n, int(cc[b]), len(C))
+        np.testing.assert_array_equal(cp[b, :len(C)], C)
+    assert int(mn[0]) == n_max and int(mn[1]) == n_max
 
 
 def test_verify_padded_tree_rows():
