@@ -92,6 +92,17 @@ int adapld_version(void);
 size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_max,
                               int Hq, int Hkv, int D);
 
+/* How adapld_tree_verify_attn decomposes a problem of these sizes (host
+ * only, no device work): info[0] waves per workgroup, info[1] waves sharing
+ * one 32-row block of stacked query rows (1, or 2: each takes half of every
+ * key tile), info[2] stacked rows per workgroup, info[3] workgroups per
+ * (sequence, kv head) along the rows, info[4] context splits (the partials
+ * of more than one are merged by a second kernel), info[5] context keys per
+ * split.  `info` is host memory of at least 6 ints, owned by the caller.
+ * Returns ADAPLD_OK, ADAPLD_ERR_NULL_ARG, or ADAPLD_ERR_INVALID_ARG /
+ * ADAPLD_ERR_UNSUPPORTED for sizes the entry point itself would reject. */
+int adapld_verify_plan(int B, int L_stride, int T_max, int Hq, int Hkv, int32_t* info);
+
 /*
  * adapld_lexical_match -- lexical anchoring (Sec. 3.3: the exact-match
  * candidate set of the query anchor, the most recent token), generalised to

@@ -38,6 +38,7 @@ SIGNATURES = {
     "adapld_last_hip_error": (ctypes.c_int, []),
     "adapld_version": (ctypes.c_int, []),
     "adapld_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int] * 9),
+    "adapld_verify_plan": (ctypes.c_int, [ctypes.c_int] * 5 + [ctypes.c_void_p]),
     "adapld_lexical_match": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
@@ -114,6 +115,13 @@ def _stream(stream):
 
 def workspace_bytes(op, B, L_stride, d=0, k=0, T_max=0, Hq=0, Hkv=0, D=0) -> int:
     return int(load_library().adapld_workspace_bytes(op, B, L_stride, d, k, T_max, Hq, Hkv, D))
+
+
+def verify_plan(B, L_stride, T_max, Hq, Hkv) -> dict:
+    """The verify kernel's decomposition for these sizes (host only)."""
+    info = (ctypes.c_int32 * 6)()
+    _check(load_library().adapld_verify_plan(B, L_stride, T_max, Hq, Hkv, info), "adapld_verify_plan")
+    return dict(zip(("waves", "kh", "rows_per_wg", "rowgroups", "nsplit", "chunk"), list(info)))
 
 
 def _i32(n, dev):

@@ -62,6 +62,20 @@ size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_m
   }
 }
 
+int adapld_verify_plan(int B, int L_stride, int T_max, int Hq, int Hkv, int32_t* info) {
+  if (!info) return ADAPLD_ERR_NULL_ARG;
+  if (B < 1 || L_stride < 1 || T_max < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv) return ADAPLD_ERR_INVALID_ARG;
+  if (T_max > ADAPLD_MAX_TREE_NODES) return ADAPLD_ERR_UNSUPPORTED;
+  const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
+  info[0] = p.waves;
+  info[1] = p.kh;
+  info[2] = p.rows_per_wg;
+  info[3] = p.rowgroups;
+  info[4] = p.nsplit;
+  info[5] = p.chunk;
+  return ADAPLD_OK;
+}
+
 int adapld_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
                          int32_t* cand_pos, int32_t* cand_count, int32_t* match_n,
                          hipStream_t stream) {

@@ -35,6 +35,7 @@ struct VerifyPlan {
   int rows_max;    // T_max * G stacked query rows per (sequence, kv head)
   int nb;          // 32-row blocks per wave
   int waves;       // waves per workgroup
+  int kh;          // waves sharing one row block (1, or 2: each takes half of every tile)
   int rows_per_wg;
   int rowgroups;
   int nsplit;      // context splits

@@ -3,10 +3,16 @@
 //
 // Work decomposition.  For one sequence b and kv head g the T*G query rows
 // (node u, query head g*G + i) are stacked as row = u*G + i, so the G heads
-// that share a kv head share every K/V byte read from HBM.  A workgroup of 4
-// or 8 waves owns waves*NB*32 stacked rows and one split of the context
-// keys; the last split also takes the tree keys.  The grid is one-dimensional
-// and XCD-aware (see the block index decode in the kernel).
+// that share a kv head share every K/V byte read from HBM.  A workgroup of 8
+// waves owns a number of 32-row blocks and one split of the context
+// keys; the last split also takes the tree keys.  Either every wave owns a
+// row block and reads both 32-key halves of each tile (KH = 1), or the two
+// waves that share a SIMD own the same row block and take one half of each
+// tile each (KH = 2): then every tile is read from LDS once per row block,
+// not once per wave, and the pair merges its two softmax states through LDS
+// at the end, so a workgroup covers twice the keys without a second split.
+// The grid is one-dimensional and XCD-aware (see the block index decode in
+// the kernel).
 //
 // Memory pipeline.  K and V tiles of 64 keys stream through a 4-stage LDS ring
 // with direct-to-LDS loads (global_load_lds_dwordx4): no VGPR staging, and up
@@ -155,9 +161,12 @@ __device__ __forceinline__ void wait_tile_and_sync(int later) {
   else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int NB, int WAVES>
+template <int NB, int WAVES, int KH>
 __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const VerifyArgs a) {
+  static_assert(KH == 1 || (KH == 2 && WAVES == 8), "wave pairs share a SIMD: waves w and w + 4");
   constexpr int kThreads = WAVES * kWave;
+  constexpr int kBlocks = WAVES / KH;   // 32-row blocks per workgroup
+  constexpr int HP = 2 / KH;            // halves of each tile one wave consumes
   constexpr int kLoadsPerWave = 2 * kTileBytes / 1024 / WAVES;   // 1 KiB per wave-wide load
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * 2 * kTileBytes];
   __shared__ uint64_t s_mask[ADAPLD_MAX_TREE_NODES * kMaskWords];
@@ -180,8 +189,11 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   const int L = min(max(a.lens[b], 0), a.L_stride);
   const int G = a.G;
   const int rows = T * G;
-  const int row_base = rg * (WAVES * NB * 32);
+  const int row_base = rg * (kBlocks * NB * 32);
   if (row_base >= rows) return;
+  // Row block of this wave, and (KH = 2) the half of every tile it takes.
+  const int wrow = KH == 2 ? wave % kBlocks : wave;
+  const int kh = KH == 2 ? wave / kBlocks : 0;
 
   const int c0 = split * a.chunk;
   const int c1 = min(c0 + a.chunk, L);
@@ -194,7 +206,7 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   int qrow[NB], qu[NB], qh[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int qr = row_base + (wave * NB + nb) * 32 + col;
+    const int qr = row_base + (wrow * NB + nb) * 32 + col;
     const bool valid = qr < rows;
     const int u = valid ? qr / G : 0;
     const int h = g * G + (qr - u * G);
@@ -260,24 +272,30 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   // Transposed V reads: each 16-lane group covers 4 keys x 16 dims; the key rows
   // are kb*32 + 16*s2 + vkey (+8), whose swizzle depends on vkey only.  vofs
   // include the offset of the V region.
+  // With KH = 2 the offsets also hold the 32-row offset of the wave's half
+  // of the tile (the swizzle has period 16 rows, so it is unchanged).
+  const int half_off = kh * 32 * kRowBytes;
   int kofs[kD / 16];
 #pragma unroll
-  for (int ds = 0; ds < kD / 16; ++ds) kofs[ds] = col * kRowBytes + (((2 * ds + half) ^ swz(col)) << 4);
+  for (int ds = 0; ds < kD / 16; ++ds)
+    kofs[ds] = half_off + col * kRowBytes + (((2 * ds + half) ^ swz(col)) << 4);
   const int vkey = 4 * half + ((lane & 15) >> 2);
   const int vdim = (lane & 16) + 4 * (lane & 3);
   int vofs[2][kD / 32];
 #pragma unroll
   for (int db = 0; db < kD / 32; ++db) {
     const int cch = (db * 32 + vdim) >> 3;
-    vofs[0][db] = kVRegion + vkey * kRowBytes + ((cch ^ swz(vkey)) << 4) + (vdim & 7) * 2;
-    vofs[1][db] = kVRegion + (vkey + 8) * kRowBytes + ((cch ^ swz(vkey + 8)) << 4) + (vdim & 7) * 2;
+    vofs[0][db] = half_off + kVRegion + vkey * kRowBytes + ((cch ^ swz(vkey)) << 4) + (vdim & 7) * 2;
+    vofs[1][db] = half_off + kVRegion + (vkey + 8) * kRowBytes + ((cch ^ swz(vkey + 8)) << 4) + (vdim & 7) * 2;
   }
   const float sl2 = a.scale_log2;
 
   static_assert(NB == 1, "software-pipelined loop handles one 32-row block per wave");
-  // Half h covers keys [32*(h&1), +32) of tile h>>1, which sits in stage (h>>1) % kStages.
+  // The wave's half h lies in tile h / HP, which sits in stage (h / HP) % kStages.
+  // With KH = 1 it covers keys [32*(h&1), +32) of that tile; with KH = 2 the
+  // wave's own half, whose offset is already in kofs and vofs.
   auto kstage = [&](int h) {
-    return (const lds_u8*)smem + ((h >> 1) & (kStages - 1)) * kTileBytes + (h & 1) * 32 * kRowBytes;
+    return (const lds_u8*)smem + ((h / HP) & (kStages - 1)) * kTileBytes + (HP == 2 ? (h & 1) : 0) * 32 * kRowBytes;
   };
   auto qk = [&](int h, f32x16_t& sacc) {
     const lds_u8* kbase = kstage(h);
@@ -288,10 +306,13 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[0][ds], sacc, 0, 0, 0);
     }
   };
-  // Fixed-half variants: HS = half index modulo 8.
-  auto qk_c = [&](auto HS, f32x16_t& sacc) {
+  // Fixed-half variants: HS = half index modulo HP * kStages.
+  auto half_base = [&](auto HS) {
     constexpr int hs = decltype(HS)::value;
-    const lds_u8* kbase = (const lds_u8*)smem + ((hs >> 1) & (kStages - 1)) * kTileBytes + (hs & 1) * 32 * kRowBytes;
+    return (const lds_u8*)smem + ((hs / HP) & (kStages - 1)) * kTileBytes + (HP == 2 ? (hs & 1) : 0) * 32 * kRowBytes;
+  };
+  auto qk_c = [&](auto HS, f32x16_t& sacc) {
+    const lds_u8* kbase = half_base(HS);
     sacc = f32x16_t{};
 #pragma unroll
     for (int ds = 0; ds < kD / 16; ++ds) {
@@ -300,8 +321,7 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
     }
   };
   auto pv_c = [&](auto HS, const bf16x8_t (&pbv)[2]) {
-    constexpr int hs = decltype(HS)::value;
-    const lds_u8* vbase = (const lds_u8*)smem + ((hs >> 1) & (kStages - 1)) * kTileBytes + (hs & 1) * 32 * kRowBytes;
+    const lds_u8* vbase = half_base(HS);
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
 #pragma unroll
@@ -331,7 +351,7 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   // Mask (masked tiles only), row max, and the lazy rescale of the running state.
   auto max_rescale = [&](int h, f32x16_t& sv, auto masked) {
     if constexpr (decltype(masked)::value) {
-      const int t = h >> 1, kb = h & 1;
+      const int t = h / HP, kb = HP == 2 ? (h & 1) : kh;
       const bool is_tree = t >= n_ctx;
       const int k0 = is_tree ? (t - n_ctx) * kKeyTile : c0 + t * kKeyTile;
       const int kend = is_tree ? T : c1;
@@ -391,9 +411,9 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
 
   // Software pipeline over halves: while the softmax of half h runs on the
   // VALU, the MFMAs of PV(h-1) and of S(h+1) are in flight.
-  const int H = 2 * n_tiles;
+  const int H = HP * n_tiles;
   const int n_plain = max(c1 - c0, 0) / kKeyTile;   // leading context tiles with no masked key
-  const int H_plain = 2 * n_plain;
+  const int H_plain = HP * n_plain;
 #pragma unroll
   for (int t = 0; t < kStages - 1; ++t)
     if (t < n_tiles) issue(t);
@@ -404,26 +424,28 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
     qk(0, s_cur);
     if (H_plain > 0) max_rescale(0, s_cur, std::false_type{});
     else max_rescale(0, s_cur, std::true_type{});
+    if (HP == 1 && H > 1) next_tile(0);   // half 1 is in tile 1
     qk(1, s_nxt);
     exp_pack(s_cur, pb);
     s_cur = s_nxt;
     auto body = [&](int h, auto masked) {
       pv(h - 1, pb);
       max_rescale(h, s_cur, masked);
-      if ((h & 1) && h + 1 < H) next_tile(h >> 1);
+      if (h % HP == HP - 1 && h + 1 < H) next_tile(h / HP);
       qk(h + 1, s_nxt);        // past the last half this reads a stale stage; unused
       exp_pack(s_cur, pb);
       s_cur = s_nxt;
     };
-    // The same step for an unmasked half whose index modulo 8 (two halves per
-    // stage, kStages stages) is the compile-time J: every LDS address is then
-    // a lane offset plus an immediate.
+    // The same step for an unmasked half whose index modulo kPeriod (HP
+    // halves per stage, kStages stages) is the compile-time J: every LDS
+    // address is then a lane offset plus an immediate.
+    constexpr int kPeriod = HP * kStages;
     auto body_c = [&](auto J, int h) {
       constexpr int j = decltype(J)::value;
-      pv_c(std::integral_constant<int, (j + 7) & 7>{}, pb);
+      pv_c(std::integral_constant<int, (j + kPeriod - 1) % kPeriod>{}, pb);
       max_rescale(h, s_cur, std::false_type{});
-      if ((j & 1) && h + 1 < H) next_tile(h >> 1);
-      qk_c(std::integral_constant<int, (j + 1) & 7>{}, s_nxt);
+      if (j % HP == HP - 1 && h + 1 < H) next_tile(h / HP);
+      qk_c(std::integral_constant<int, (j + 1) % kPeriod>{}, s_nxt);
       exp_pack(s_cur, pb);
       s_cur = s_nxt;
     };
@@ -436,15 +458,25 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
     using I7 = std::integral_constant<int, 7>;
     using I0 = std::integral_constant<int, 0>;
     int h = 1;
-    for (; h + 8 <= H_plain; h += 8) {   // h = 1 (mod 8) here
-      body_c(I1{}, h);
-      body_c(I2{}, h + 1);
-      body_c(I3{}, h + 2);
-      body_c(I4{}, h + 3);
-      body_c(I5{}, h + 4);
-      body_c(I6{}, h + 5);
-      body_c(I7{}, h + 6);
-      body_c(I0{}, h + 7);
+    if constexpr (kPeriod == 8) {
+      for (; h + 8 <= H_plain; h += 8) {   // h = 1 (mod 8) here
+        body_c(I1{}, h);
+        body_c(I2{}, h + 1);
+        body_c(I3{}, h + 2);
+        body_c(I4{}, h + 3);
+        body_c(I5{}, h + 4);
+        body_c(I6{}, h + 5);
+        body_c(I7{}, h + 6);
+        body_c(I0{}, h + 7);
+      }
+    } else {
+      static_assert(kPeriod == 4, "one or two halves per tile, four stages");
+      for (; h + 4 <= H_plain; h += 4) {   // h = 1 (mod 4) here
+        body_c(I1{}, h);
+        body_c(I2{}, h + 1);
+        body_c(I3{}, h + 2);
+        body_c(I0{}, h + 3);
+      }
     }
     for (; h < H_plain; ++h) body(h, std::false_type{});
     for (; h < H; ++h) body(h, std::true_type{});
@@ -452,14 +484,53 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   }
 
   // Epilogue: lane holds dims db*32 + 8*(r/4) + 4*half + r%4 of its query row.
+  float l_tot[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) l_tot[nb] = l_run[nb] + __shfl_xor(l_run[nb], 32, kWave);
+  if constexpr (KH == 2) {
+    // The pair (wrow, kh = 1) hands its state to (wrow, kh = 0) through the
+    // ring, which no wave reads any more after this barrier; lane i of both
+    // waves holds the same query column.  Each state is relative to its own
+    // running max: the merged one takes M = max(m0, m1) and weights 2^(m - M).
+    static_assert(NB == 1, "one row block per wave");
+    float4* xo = reinterpret_cast<float4*>(smem);                        // [kBlocks][16][64]
+    float2* xml = reinterpret_cast<float2*>(smem + kBlocks * 16 * 64 * 16);   // [kBlocks][64]
+    __syncthreads();
+    if (kh == 1) {
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          xo[(wrow * 16 + db * 4 + r4) * 64 + lane] =
+              make_float4(o[0][db][4 * r4], o[0][db][4 * r4 + 1], o[0][db][4 * r4 + 2], o[0][db][4 * r4 + 3]);
+      xml[wrow * 64 + lane] = make_float2(m_run[0], l_tot[0]);
+    }
+    __syncthreads();
+    if (kh == 1) return;
+    const float2 ml = xml[wrow * 64 + lane];
+    const float M = fmaxf(m_run[0], ml.x);
+    const float a0 = m_run[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[0] - M);
+    const float a1 = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const float4 v = xo[(wrow * 16 + db * 4 + r4) * 64 + lane];
+        o[0][db][4 * r4 + 0] = a0 * o[0][db][4 * r4 + 0] + a1 * v.x;
+        o[0][db][4 * r4 + 1] = a0 * o[0][db][4 * r4 + 1] + a1 * v.y;
+        o[0][db][4 * r4 + 2] = a0 * o[0][db][4 * r4 + 2] + a1 * v.z;
+        o[0][db][4 * r4 + 3] = a0 * o[0][db][4 * r4 + 3] + a1 * v.w;
+      }
+    l_tot[0] = a0 * l_tot[0] + a1 * ml.y;
+    m_run[0] = M;
+  }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int qr = qrow[nb];
-    const float l_tot = l_run[nb] + __shfl_xor(l_run[nb], 32, kWave);
     if (qr >= rows) continue;
     const int u = qu[nb], h = qh[nb];
     if (a.nsplit == 1) {
-      const float inv = 1.f / l_tot;
+      const float inv = 1.f / l_tot[nb];
       uint16_t* op = a.out + (((size_t)b * a.T_max + u) * a.Hq + h) * kD;
 #pragma unroll
       for (int db = 0; db < kD / 32; ++db)
@@ -471,10 +542,10 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
           pk.y = f32_to_bf16_bits(o[nb][db][4 * r4 + 2] * inv) | (f32_to_bf16_bits(o[nb][db][4 * r4 + 3] * inv) << 16);
           *reinterpret_cast<uint2*>(op + dim) = pk;
         }
-      if (half == 0 && a.lse) a.lse[((size_t)b * a.Hq + h) * a.T_max + u] = (m_run[nb] + log2f(l_tot)) * kLn2;
+      if (half == 0 && a.lse) a.lse[((size_t)b * a.Hq + h) * a.T_max + u] = (m_run[nb] + log2f(l_tot[nb])) * kLn2;
     } else {
       const size_t slot = ((size_t)bg * a.nsplit + split) * a.rows_max + qr;
-      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      const float inv = l_tot[nb] > 0.f ? 1.f / l_tot[nb] : 0.f;
       uint16_t* wp = a.ws_o + slot * kD;
 #pragma unroll
       for (int db = 0; db < kD / 32; ++db)
@@ -486,7 +557,7 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
           pk.y = f32_to_bf16_bits(o[nb][db][4 * r4 + 2] * inv) | (f32_to_bf16_bits(o[nb][db][4 * r4 + 3] * inv) << 16);
           *reinterpret_cast<uint2*>(wp + dim) = pk;
         }
-      if (half == 0) a.ws_ml[slot] = make_float2(m_run[nb], l_tot);
+      if (half == 0) a.ws_ml[slot] = make_float2(m_run[nb], l_tot[nb]);
     }
   }
 }
@@ -547,28 +618,52 @@ __global__ __launch_bounds__(256) void verify_combine_kernel(const VerifyArgs a)
 }  // namespace
 
 VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv) {
-  VerifyPlan p{};
-  p.G = Hq / Hkv;
-  p.rows_max = T_max * p.G;
-  // 8 waves x one 32-row block (two waves per SIMD, so one wave's softmax and
-  // LDS waits overlap the other's MFMAs); small trees use 4 waves.
-  const int blocks = (p.rows_max + 31) / 32;
-  p.nb = 1;
-  p.waves = blocks > 4 ? 8 : 4;
-  p.rows_per_wg = p.waves * p.nb * 32;
-  p.rowgroups = (p.rows_max + p.rows_per_wg - 1) / p.rows_per_wg;
-  // About one workgroup per CU (256 CUs), splits no shorter than four tiles:
-  // small batches split the context finely, since a workgroup's time is then
-  // mostly the latency of its first tiles.
-  const int base = std::max(1, B * Hkv * p.rowgroups);
-  const int want = std::max(1, (256 + base - 1) / base);
+  // Candidates: 8 waves each owning a 32-row block (256 rows per workgroup),
+  // or 8 waves in SIMD pairs sharing a row block (128 rows, each wave half of
+  // every tile).  Both keep two waves per SIMD, so one wave's softmax and LDS
+  // waits overlap the other's MFMAs.  For each, and each number of context
+  // splits, the estimated time is the
+  // number of rounds of workgroups over the 256 CUs (one workgroup per CU:
+  // the LDS ring takes 128 KiB) times one workgroup's time, which is its
+  // per-SIMD share of row x key work plus a fixed start-up cost, plus the
+  // combine kernel when the context is split.  The constants are in units of
+  // one SIMD's time for 32 rows x 64 keys with two waves per SIMD.
+  constexpr double kStartTiles = 12.0;    // start-up and drain of one workgroup
+  constexpr double kCombineTiles = 10.0;  // the combine launch and its traffic
+  struct Cand { int waves, kh; double per_tile; };   // per_tile: SIMD cost of one 64-key tile
+  const Cand cands[] = {{8, 1, 2.0}, {8, 2, 1.0}};
+  const int G = Hq / Hkv;
+  const int rows_max = T_max * G;
   const int max_split = std::max(1, (L_stride + 4 * kKeyTile - 1) / (4 * kKeyTile));
-  p.nsplit = std::min(want, max_split);
-  int chunk = (L_stride + p.nsplit - 1) / p.nsplit;
-  chunk = ((chunk + kKeyTile - 1) / kKeyTile) * kKeyTile;
-  p.chunk = std::max(chunk, kKeyTile);
-  p.nsplit = std::max(1, (L_stride + p.chunk - 1) / p.chunk);
-  return p;
+  VerifyPlan best{};
+  double best_cost = 0.0;
+  for (const Cand& c : cands) {
+    const int rows_per_wg = c.waves / c.kh * 32;
+    const int rowgroups = (rows_max + rows_per_wg - 1) / rows_per_wg;
+    for (int want = 1; want <= max_split; ++want) {
+      int chunk = (L_stride + want - 1) / want;
+      chunk = std::max(((chunk + kKeyTile - 1) / kKeyTile) * kKeyTile, kKeyTile);
+      const int nsplit = std::max(1, (L_stride + chunk - 1) / chunk);
+      if (nsplit != want) continue;   // the same split as a smaller count
+      const long wgs = (long)B * Hkv * rowgroups * nsplit;
+      const long rounds = (wgs + 255) / 256;
+      const double tiles = (double)chunk / kKeyTile + (T_max + kKeyTile - 1) / kKeyTile;
+      const double cost = rounds * (c.per_tile * tiles + kStartTiles) + (nsplit > 1 ? kCombineTiles : 0.0);
+      if (best.waves == 0 || cost < best_cost) {
+        best_cost = cost;
+        best.G = G;
+        best.rows_max = rows_max;
+        best.nb = 1;
+        best.waves = c.waves;
+        best.kh = c.kh;
+        best.rows_per_wg = rows_per_wg;
+        best.rowgroups = rowgroups;
+        best.nsplit = nsplit;
+        best.chunk = chunk;
+      }
+    }
+  }
+  return best;
 }
 
 size_t verify_ws_bytes(const VerifyPlan& p, int B, int Hkv) {
@@ -597,10 +692,10 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
   a.rowgroups = p.rowgroups;
   a.n_kvgroups = B * Hkv * p.nsplit;
   const dim3 grid(((a.n_kvgroups + 7) / 8) * 8 * p.rowgroups);
-  if (p.waves == 8)
-    hipLaunchKernelGGL((tree_verify_kernel<1, 8>), grid, dim3(8 * kWave), 0, stream, a);
+  if (p.kh == 2)
+    hipLaunchKernelGGL((tree_verify_kernel<1, 8, 2>), grid, dim3(8 * kWave), 0, stream, a);
   else
-    hipLaunchKernelGGL((tree_verify_kernel<1, 4>), grid, dim3(4 * kWave), 0, stream, a);
+    hipLaunchKernelGGL((tree_verify_kernel<1, 8, 1>), grid, dim3(8 * kWave), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.nsplit == 1) return e;
   hipLaunchKernelGGL(verify_combine_kernel, dim3((p.rows_max + 7) / 8, B * Hkv), dim3(256), 0, stream, a);

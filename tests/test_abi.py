@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 8
+    assert len(names) == 9
     for n in names:
         assert hasattr(lib, n), n
         assert n in binding.SIGNATURES, n
@@ -50,9 +50,30 @@ def test_workspace_sizes(lib):
     assert sem == 16 * 1024 * 8 * 8                                # one list per scan wave (1024) and sequence
     assert ws(2, 16, 300, 4096, 8, 0, 0, 0, 0) == 16 * 300 * 8 * 8  # at most one per row
     assert ws(2, 16, 8192, 4096, 65, 0, 0, 0, 0) == 0              # k beyond the limit
-    assert ws(4, 16, 8192, 0, 0, 52, 32, 8, 128) > 0               # split context
+    assert ws(4, 1, 4096, 0, 0, 44, 32, 8, 128) > 0                # split context
+    assert ws(4, 16, 8192, 0, 0, 52, 32, 8, 128) == 0              # one split: no partials
     assert ws(4, 16, 8192, 0, 0, 52, 32, 7, 128) == 0              # Hq % Hkv != 0
     assert ws(9, 16, 8192, 0, 0, 52, 32, 8, 128) == 0
+
+
+def test_verify_plan(lib):
+    info = (ctypes.c_int32 * 6)()
+    f = lib.adapld_verify_plan
+    assert f(16, 8192, 52, 32, 8, N) == NULL
+    assert f(0, 8192, 52, 32, 8, info) == INVALID
+    assert f(16, 8192, 52, 32, 7, info) == INVALID
+    assert f(16, 8192, 257, 32, 8, info) == UNSUPPORTED
+    assert f(16, 8192, 52, 32, 8, info) == OK
+    waves, kh, rows_per_wg, rowgroups, nsplit, chunk = list(info)
+    assert rows_per_wg == waves // kh * 32 and rowgroups * rows_per_wg >= 52 * 4
+    assert nsplit * chunk >= 8192 and chunk % 64 == 0
+    # the shapes of test_verify_variants (tests/test_gpu_parity.py) take all
+    # four decompositions: (waves per row block, split context)
+    seen = set()
+    for B, L, T, Hq, Hkv in ((12, 300, 52, 40, 8), (6, 1200, 36, 32, 8), (1, 300, 20, 8, 2), (1, 1200, 20, 8, 2)):
+        p = binding.verify_plan(B, L, T, Hq, Hkv)
+        seen.add((p["kh"], p["nsplit"] > 1))
+    assert seen == {(1, False), (1, True), (2, False), (2, True)}
 
 
 def test_lexical_validation(lib):

@@ -179,6 +179,26 @@ def test_lexical_single_piece_runs(L, n_max):
     assert int(mn[0]) == n_max and int(mn[1]) == n_max
 
 
+# Shapes that take each verify decomposition (tests/test_abi.py checks the
+# plan): 256-row workgroups whole and split, 128-row wave-pair workgroups
+# whole and split.  The first has 260 stacked rows, so its second row group
+# holds 4 valid rows.
+VERIFY_VARIANTS = {
+    "rows256_whole": dict(B=12, L=300, d=128, Hq=40, Hkv=8, k=8, W=4, S=12, n_max=3, seed=101, forced_every=3),
+    "rows256_split": dict(B=6, L=1200, d=128, Hq=32, Hkv=8, k=8, W=4, S=8, n_max=3, seed=102, forced_every=2),
+    "pairs_whole": dict(B=1, L=300, d=128, Hq=8, Hkv=2, k=4, W=4, S=4, n_max=3, seed=103),
+    "pairs_split": dict(B=1, L=1200, d=128, Hq=8, Hkv=2, k=4, W=4, S=4, n_max=3, seed=104),
+}
+
+
+@pytest.mark.parametrize("name", list(VERIFY_VARIANTS))
+def test_verify_variants(name):
+    cfg = small_config(**VERIFY_VARIANTS[name])
+    x = make_inputs(cfg)
+    g = run_step(cfg, upload(x))
+    check_all(cfg, x, g, ctx=name)
+
+
 def test_verify_padded_tree_rows():
     """T_max above W(S+1): the padding rows of q, k_tree and v_tree are ignored."""
     cfg = small_config(B=3, L=700, d=256, Hq=8, Hkv=2, k=8, W=3, S=4, n_max=3, seed=94, forced_every=2)
