@@ -417,7 +417,16 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
 #pragma unroll
   for (int t = 0; t < kStages - 1; ++t)
     if (t < n_tiles) issue(t);
-  if (H > 0) {
+  // A wave whose row block holds no valid row (the tail of the last row
+  // group) issues its share of every tile and takes every barrier, and does
+  // no math: its MFMAs would only cost power.
+  const bool idle = row_base + wrow * NB * 32 >= rows;
+  if (idle && H > 0) {
+    wait_tile_and_sync<kLoadsPerWave>(min(kStages - 2, n_tiles - 1));
+    if (HP == 1 && H > 1) next_tile(0);
+    for (int h = 1; h < H; ++h)
+      if (h % HP == HP - 1 && h + 1 < H) next_tile(h / HP);
+  } else if (H > 0) {
     f32x16_t s_cur, s_nxt;
     bf16x8_t pb[2];
     wait_tile_and_sync<kLoadsPerWave>(min(kStages - 2, n_tiles - 1));
