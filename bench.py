@@ -30,9 +30,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "211eda1159ca34ad42302b8847d42d9ad20caeeb8db368a49396b5b0cc3ee865",
-    "fetch_kib": 269001.1 + 7100.6,
-    "write_kib": 10939.5 + 5628.0,
+    "source_sha256": "55cc72f9917459d76ea7e024f8e519ce8e7b921110f33a4cf8b72b2c3fe57a0c",
+    "fetch_kib": 268951.9,
+    "write_kib": 5392.1,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
 }

@@ -356,10 +356,13 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
       const int k0 = is_tree ? (t - n_ctx) * kKeyTile : c0 + t * kKeyTile;
       const int kend = is_tree ? T : c1;
       const uint64_t mword = (is_tree && qrow[0] < rows) ? s_mask[qu[0] * a.nw + (k0 >> 6)] : 0ull;
+      // Bit 8*(r/4) + r%4 of mbits is the mask bit of this lane's key r.
+      const uint32_t mbits = (uint32_t)(mword >> (kb * 32 + 4 * half));
+      const int kbase = k0 + kb * 32 + 4 * half;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int kk = kb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);   // key within the tile
-        const bool ok = k0 + kk < kend && (!is_tree || ((mword >> kk) & 1ull));
+        const int kr = 8 * (r >> 2) + (r & 3);   // key kbase + kr
+        const bool ok = kbase + kr < kend && (!is_tree || ((mbits >> kr) & 1u));
         sv[r] = ok ? sv[r] : -INFINITY;
       }
     }
