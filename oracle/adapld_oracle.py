@@ -20,6 +20,12 @@ Four steps, per sequence, in the paper's order (Sec. 3.3 - 3.6, Algorithm 1):
                        each a copied span; an ancestor-or-self mask.
 ``tree_verify_attn``-- tree-masked attention over the KV cache (Sec. 3.6,
                        tree attention after Medusa), softmax in float64.
+``accept_greedy``   -- greedy verification of the tree (Sec. 3.6 and the
+                       speculative-decoding background of Appendix A: with
+                       greedy decoding a draft token is kept when it equals
+                       the target's own choice, up to the first mismatch),
+                       and ``compact_kv`` -- the accepted nodes' K/V moved to
+                       consecutive cache positions after the context.
 
 Readings of the paper used here (where it is silent, ambiguous or where the
 reproduced workload differs from its text):
@@ -41,7 +47,18 @@ reproduced workload differs from its text):
   a depth-0 node is -1 (the root, the last context token, lives in the KV
   cache and is not a query row);
 * verification keys for node u are all context keys 0..L-1 followed by the
-  tree keys of u's ancestors-or-self in ascending node order.
+  tree keys of u's ancestors-or-self in ascending node order;
+* greedy acceptance takes the target's greedy token after the context (the
+  root) and after every node as given (no model here); node u is accepted
+  when its token equals the target's token after its parent and every
+  ancestor is accepted; the accepted path ends at the deepest accepted node
+  (lowest index among equally deep ones, which only duplicate sibling tokens
+  can produce); the emitted tokens are the path's tokens followed by the
+  target's token after its last node (the bonus token; the target's token
+  after the context when nothing is accepted);
+* the accepted nodes' K/V go to cache positions L, L+1, ... in path order;
+  positions at or beyond the cache capacity are not written.  The bonus
+  token's K/V come from the next forward pass, outside this step.
 
 Parity unpinned: none of the paper's printed numbers can pin these functions
 (the paper prints no worked example); every function is pinned by brute force,
@@ -224,6 +241,65 @@ def tree_verify_attn(Q, Kc, Vc, Kt, Vt, mask, L: int, scale: float):
                 O[u, h] = (e @ vals) / l
                 LSE[h, u] = m + np.log(l)
     return O, LSE
+
+
+# --------------------------------------------------------------------------
+# Step 5: greedy acceptance and KV compaction (Sec. 3.6; Appendix A)
+# --------------------------------------------------------------------------
+
+def accept_greedy(token, parent, root_next: int, node_next):
+    """Greedy verification of a draft tree.
+
+    token[u], parent[u]: the tree (parent -1 for depth-0 nodes).  root_next:
+    the target's greedy token after the context; node_next[u]: its greedy
+    token after node u's path.  Every root-to-node path is walked from the
+    root: it survives while each node's token equals the target's token after
+    the previous node.  Returns (path, emitted): the node list of the deepest
+    surviving path (depth 0 first; lowest end index among equally deep ones)
+    and the emitted tokens, the path's tokens followed by the bonus token.
+    """
+    T = len(token)
+    best, best_len = None, 0
+    for u in range(T):
+        chain = []
+        v = u
+        while v != -1:
+            chain.append(v)
+            v = int(parent[v])
+        chain.reverse()
+        expected = int(root_next)
+        ok = True
+        for v in chain:
+            if int(token[v]) != expected:
+                ok = False
+                break
+            expected = int(node_next[v])
+        if ok and len(chain) > best_len:
+            best, best_len = u, len(chain)
+    path = []
+    v = best if best is not None else -1
+    while v != -1:
+        path.append(v)
+        v = int(parent[v])
+    path.reverse()
+    bonus = int(node_next[best]) if best is not None else int(root_next)
+    emitted = [int(token[v]) for v in path] + [bonus]
+    return path, emitted
+
+
+def compact_kv(kc_bits, vc_bits, kt_bits, vt_bits, L: int, path):
+    """The cache after acceptance: copies of Kc, Vc ((Hkv, L_stride, D) bit
+    patterns) with row L+i of every kv head replaced by Kt[path[i]], Vt[path[i]]
+    ((T, Hkv, D)), for L+i < L_stride."""
+    K = np.array(kc_bits, copy=True)
+    V = np.array(vc_bits, copy=True)
+    cap = K.shape[1]
+    for i, u in enumerate(path):
+        if L + i >= cap:
+            break
+        K[:, L + i] = kt_bits[u]
+        V[:, L + i] = vt_bits[u]
+    return K, V
 
 
 # --------------------------------------------------------------------------

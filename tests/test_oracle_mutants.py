@@ -13,7 +13,7 @@ from concurrent.futures import ThreadPoolExecutor
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle_lexical.py", "tests/test_oracle_semantic.py",
-        "tests/test_oracle_tree.py", "tests/test_oracle_verify.py"]
+        "tests/test_oracle_tree.py", "tests/test_oracle_verify.py", "tests/test_oracle_accept.py"]
 
 MUTANTS = [
     ("js = np.arange(n - 1, L - 1)", "js = np.arange(n - 1, L)"),              # anchor counts itself
@@ -35,6 +35,11 @@ MUTANTS = [
     ("LSE[h, u] = m + np.log(l)", "LSE[h, u] = np.log(l)"),                   # max dropped
     ("heads = range(g * G, (g + 1) * G)", "heads = range(g, Hq, Hkv)"),       # wrong GQA grouping
     ("O[u, h] = (e @ vals) / l", "O[u, h] = (e @ vals)"),                       # no normalisation
+    ("            expected = int(node_next[v])\n", "            expected = int(node_next[u])\n"),  # end node's choice
+    ("        if ok and len(chain) > best_len:", "        if ok and len(chain) >= best_len:"),  # ties to the last end
+    ("    bonus = int(node_next[best]) if best is not None else int(root_next)", "    bonus = int(root_next)"),
+    ("        chain.reverse()\n", ""),                                         # walks the path bottom-up
+    ("        K[:, L + i] = kt_bits[u]", "        K[:, L + i] = kt_bits[i]"),  # rows by rank, not node
 ]
 
 
