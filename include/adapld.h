@@ -13,6 +13,12 @@
  *                               (Sec. 3.5, Sec. 3.6)
  *   4. adapld_tree_verify_attn  tree-masked verify attention (Sec. 3.6)
  *
+ * and, once the target's greedy tokens for the verified tree are known,
+ *
+ *   5. adapld_accept_greedy     greedy acceptance of the tree and compaction
+ *                               of the accepted nodes' K/V (Sec. 3.6,
+ *                               Appendix A)
+ *
  * Conventions shared by every entry point
  * ---------------------------------------
  * - Every pointer argument is DEVICE memory owned by the caller.  The library
@@ -233,6 +239,50 @@ int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint
                             int L_stride, int T_max, int Hq, int Hkv, int D, float scale,
                             uint16_t* out, float* lse, void* ws, size_t ws_bytes,
                             hipStream_t stream);
+
+/*
+ * adapld_accept_greedy -- greedy verification of the draft tree (Sec. 3.6:
+ * verification follows the standard speculative-decoding rule; Appendix A:
+ * with greedy decoding a draft token is kept when it equals the target's own
+ * choice, and the first mismatch ends it) and compaction of the kept nodes'
+ * K/V into the cache.
+ *
+ * Inputs (the tree as adapld_build_draft_tree writes it):
+ *   node_token, node_parent, node_depth  int32 [B, T_max]
+ *   node_count  int32 [B]   (clamped to [0, T_max] on the device)
+ *   tree_mask   uint64 [B, T_max, ceil(T_max/64)]  ancestor-or-self bits
+ *   target_next int32 [B, T_max + 1]: column 0 = the target's greedy token
+ *               after the context, column 1 + u = after node u's path
+ *   lens        int32 [B]   context length L (clamped to [0, L_stride])
+ *   k_tree, v_tree  bf16 [B, T_max, Hkv, D]   the tree's K/V (verify layout)
+ * Node u is kept when its token equals the target's token after its parent
+ * (after the context for a depth-0 node) and so is every ancestor's; the
+ * kept path ends at the deepest kept node (the lowest index among equally
+ * deep ones).
+ * Outputs:
+ *   accept_len   int32 [B]               n = number of kept draft nodes
+ *   accept_nodes int32 [B, T_max]        entries 0..n-1: the kept nodes by depth
+ *   out_tokens   int32 [B, T_max + 1]    entries 0..n: the kept tokens, then
+ *                the bonus token (the target's token after the last kept
+ *                node, or after the context when n = 0)
+ *   k_ctx, v_ctx bf16 [B, Hkv, L_stride, D]: rows L .. L+n-1 of every kv head
+ *                receive the kept nodes' K/V rows in path order; rows at or
+ *                beyond L_stride are not written; other rows are untouched.
+ *                The bonus token's K/V come from the next forward pass.
+ * k_tree, v_tree, k_ctx and v_ctx are either all given (D must be 128, each
+ * 16-byte aligned) or all NULL (acceptance only; Hkv and D are then ignored).
+ * Entries past n in accept_nodes and past n+1 in out_tokens are unspecified.
+ * Errors: NULL_ARG (a required pointer, or some but not all of the four K/V
+ * pointers); INVALID_ARG (B < 0, L_stride < 1, T_max < 1, Hkv < 1 with K/V,
+ * misaligned K/V); UNSUPPORTED (T_max > ADAPLD_MAX_TREE_NODES, D != 128).
+ */
+int adapld_accept_greedy(const int32_t* node_token, const int32_t* node_parent,
+                         const int32_t* node_depth, const int32_t* node_count,
+                         const uint64_t* tree_mask, const int32_t* target_next, const int32_t* lens,
+                         const uint16_t* k_tree, const uint16_t* v_tree, int B, int L_stride,
+                         int T_max, int Hkv, int D, int32_t* accept_len, int32_t* accept_nodes,
+                         int32_t* out_tokens, uint16_t* k_ctx, uint16_t* v_ctx,
+                         hipStream_t stream);
 
 #ifdef __cplusplus
 }

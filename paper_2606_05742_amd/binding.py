@@ -39,6 +39,7 @@ SIGNATURES = {
     "adapld_version": (ctypes.c_int, []),
     "adapld_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int] * 9),
     "adapld_verify_plan": (ctypes.c_int, [ctypes.c_int] * 5 + [ctypes.c_void_p]),
+    "adapld_accept_greedy": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 5 + [ctypes.c_void_p] * 6),
     "adapld_lexical_match": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
@@ -224,6 +225,43 @@ def tree_verify_attn(q, k_ctx, v_ctx, k_tree, v_tree, lens, node_count, tree_mas
         _ptr(ws, "ws", (torch.uint8,)), ws.numel(), _stream(stream))
     _check(st, "adapld_tree_verify_attn")
     return out, lse
+
+
+def accept_greedy(node_token, node_parent, node_depth, node_count, tree_mask, target_next, lens, *,
+                  k_tree=None, v_tree=None, k_ctx=None, v_ctx=None, accept_len=None, accept_nodes=None,
+                  out_tokens=None, stream=None):
+    """Greedy acceptance of the draft tree and, when the four K/V tensors are
+    given, compaction of the kept nodes' K/V into k_ctx / v_ctx (in place).
+    Returns (accept_len, accept_nodes, out_tokens)."""
+    lib = load_library()
+    B, T_max = node_token.shape
+    dev = node_token.device
+    nw = (T_max + 63) // 64
+    kv = (k_tree, v_tree, k_ctx, v_ctx)
+    if any(t is not None for t in kv) and not all(t is not None for t in kv):
+        raise AdapldError(-1, "accept_greedy: give all of k_tree, v_tree, k_ctx, v_ctx or none")
+    Hkv, D, L_stride = 0, HEAD_DIM, 1
+    if k_ctx is not None:
+        Hkv, L_stride, D = k_ctx.shape[1], k_ctx.shape[2], k_ctx.shape[3]
+    accept_len = torch.empty(B, dtype=torch.int32, device=dev) if accept_len is None else accept_len
+    accept_nodes = torch.empty((B, T_max), dtype=torch.int32, device=dev) if accept_nodes is None else accept_nodes
+    out_tokens = torch.empty((B, T_max + 1), dtype=torch.int32, device=dev) if out_tokens is None else out_tokens
+    i32 = (torch.int32,)
+    st = lib.adapld_accept_greedy(
+        _ptr(node_token, "node_token", i32, (B, T_max)), _ptr(node_parent, "node_parent", i32, (B, T_max)),
+        _ptr(node_depth, "node_depth", i32, (B, T_max)), _ptr(node_count, "node_count", i32, (B,)),
+        _ptr(tree_mask, "tree_mask", (torch.int64, torch.uint64), (B, T_max, nw)),
+        _ptr(target_next, "target_next", i32, (B, T_max + 1)), _ptr(lens, "lens", i32, (B,)),
+        _ptr(k_tree, "k_tree", _BF16_DTYPES, (B, T_max, Hkv, D), nullable=True),
+        _ptr(v_tree, "v_tree", _BF16_DTYPES, (B, T_max, Hkv, D), nullable=True),
+        B, L_stride, T_max, Hkv, D,
+        _ptr(accept_len, "accept_len", i32, (B,)), _ptr(accept_nodes, "accept_nodes", i32, (B, T_max)),
+        _ptr(out_tokens, "out_tokens", i32, (B, T_max + 1)),
+        _ptr(k_ctx, "k_ctx", _BF16_DTYPES, (B, Hkv, L_stride, D), nullable=True),
+        _ptr(v_ctx, "v_ctx", _BF16_DTYPES, (B, Hkv, L_stride, D), nullable=True),
+        _stream(stream))
+    _check(st, "adapld_accept_greedy")
+    return accept_len, accept_nodes, out_tokens
 
 
 @dataclass

@@ -156,4 +156,32 @@ int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint
                                                     Hkv, scale, out, lse, ws, p, stream));
 }
 
+int adapld_accept_greedy(const int32_t* node_token, const int32_t* node_parent,
+                         const int32_t* node_depth, const int32_t* node_count,
+                         const uint64_t* tree_mask, const int32_t* target_next, const int32_t* lens,
+                         const uint16_t* k_tree, const uint16_t* v_tree, int B, int L_stride,
+                         int T_max, int Hkv, int D, int32_t* accept_len, int32_t* accept_nodes,
+                         int32_t* out_tokens, uint16_t* k_ctx, uint16_t* v_ctx,
+                         hipStream_t stream) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!node_token || !node_parent || !node_depth || !node_count || !tree_mask || !target_next ||
+      !lens || !accept_len || !accept_nodes || !out_tokens)
+    return ADAPLD_ERR_NULL_ARG;
+  const int n_kv = (k_tree != nullptr) + (v_tree != nullptr) + (k_ctx != nullptr) + (v_ctx != nullptr);
+  if (n_kv != 0 && n_kv != 4) return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || T_max < 1) return ADAPLD_ERR_INVALID_ARG;
+  if (T_max > ADAPLD_MAX_TREE_NODES || (int64_t)B * (T_max + 1) > INT32_MAX) return ADAPLD_ERR_UNSUPPORTED;
+  if (n_kv == 4) {
+    if (Hkv < 1) return ADAPLD_ERR_INVALID_ARG;
+    if (D != ADAPLD_HEAD_DIM) return ADAPLD_ERR_UNSUPPORTED;
+    if (misaligned16(k_tree) || misaligned16(v_tree) || misaligned16(k_ctx) || misaligned16(v_ctx))
+      return ADAPLD_ERR_INVALID_ARG;
+  }
+  return hip_status(adapld::launch_accept_greedy(node_token, node_parent, node_depth, node_count,
+                                                 tree_mask, target_next, lens, k_tree, v_tree, B,
+                                                 L_stride, T_max, n_kv ? Hkv : 0, accept_len,
+                                                 accept_nodes, out_tokens, k_ctx, v_ctx, stream));
+}
+
 }  // extern "C"

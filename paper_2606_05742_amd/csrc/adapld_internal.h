@@ -71,4 +71,12 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
                                    int Hq, int Hkv, float scale, uint16_t* out, float* lse,
                                    void* ws, const VerifyPlan& plan, hipStream_t stream);
 
+hipError_t launch_accept_greedy(const int32_t* node_token, const int32_t* node_parent,
+                                const int32_t* node_depth, const int32_t* node_count,
+                                const uint64_t* tree_mask, const int32_t* target_next,
+                                const int32_t* lens, const uint16_t* k_tree, const uint16_t* v_tree,
+                                int B, int L_stride, int T_max, int Hkv, int32_t* accept_len,
+                                int32_t* accept_nodes, int32_t* out_tokens, uint16_t* k_ctx,
+                                uint16_t* v_ctx, hipStream_t stream);
+
 }  // namespace adapld

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 9
+    assert len(names) == 10
     for n in names:
         assert hasattr(lib, n), n
         assert n in binding.SIGNATURES, n
@@ -74,6 +74,24 @@ def test_verify_plan(lib):
         p = binding.verify_plan(B, L, T, Hq, Hkv)
         seen.add((p["kh"], p["nsplit"] > 1))
     assert seen == {(1, False), (1, True), (2, False), (2, True)}
+
+
+def test_accept_validation(lib):
+    f = lib.adapld_accept_greedy
+    A = [P] * 7            # node_token, node_parent, node_depth, node_count, tree_mask, target_next, lens
+    O = [P, P, P]          # accept_len, accept_nodes, out_tokens
+    assert f(*A, N, N, 0, 0, 0, 0, 0, *O, N, N, N) == OK                 # B = 0: nothing to do
+    assert f(*A, N, N, -1, 8, 8, 0, 0, *O, N, N, N) == INVALID
+    assert f(N, *A[1:], N, N, 2, 8, 8, 0, 0, *O, N, N, N) == NULL
+    assert f(*A, N, N, 2, 8, 8, 0, 0, P, P, N, N, N, N) == NULL          # out_tokens missing
+    assert f(*A, P, N, 2, 8, 8, 2, 128, *O, P, P, N) == NULL             # some but not all K/V
+    assert f(*A, N, N, 2, 0, 8, 0, 0, *O, N, N, N) == INVALID           # L_stride < 1
+    assert f(*A, N, N, 2, 8, 0, 0, 0, *O, N, N, N) == INVALID           # T_max < 1
+    assert f(*A, N, N, 2, 8, 257, 0, 0, *O, N, N, N) == UNSUPPORTED
+    assert f(*A, P, P, 2, 8, 8, 0, 128, *O, P, P, N) == INVALID          # Hkv < 1 with K/V
+    assert f(*A, P, P, 2, 8, 8, 2, 64, *O, P, P, N) == UNSUPPORTED       # D != 128
+    Q = ctypes.c_void_p(0x10008)                                          # 8-byte aligned only
+    assert f(*A, Q, P, 2, 8, 8, 2, 128, *O, P, P, N) == INVALID
 
 
 def test_lexical_validation(lib):
