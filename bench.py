@@ -166,6 +166,74 @@ def main():
         print(json.dumps(rec), flush=True)
 
 
+def plant_targets(node_token, node_parent, node_count, T_max, seed=0):
+    """The target's greedy tokens for the acceptance measurement: per sequence
+    a random root path kept for a random number of steps, every other entry a
+    token of the tree (so chance matches occur)."""
+    rng = np.random.default_rng(seed)
+    B = node_token.shape[0]
+    tn = np.zeros((B, T_max + 1), dtype=np.int32)
+    for b in range(B):
+        T = int(node_count[b])
+        tok, par = node_token[b, :T], node_parent[b, :T]
+        pool = list(tok) if T else [0]
+        tn[b] = rng.choice(pool, size=T_max + 1)
+        if T:
+            v, path = int(rng.integers(0, T)), []
+            while v != -1:
+                path.append(v)
+                v = int(par[v])
+            path.reverse()
+            j = int(rng.integers(0, len(path) + 1))
+            if j:
+                tn[b, 0] = tok[path[0]]
+                for i in range(j - 1):
+                    tn[b, 1 + path[i]] = tok[path[i + 1]]
+    return tn
+
+
+def measure_accept(adapld, cfg, bufs, s, lens_np, lens, node_count, steps, stream):
+    """Greedy acceptance + KV compaction after the step (not part of the
+    step's time): HIP events around each call, and its algorithmic bytes."""
+    import torch
+    nt, npar = bufs.node_token.cpu().numpy(), bufs.node_parent.cpu().numpy()
+    tn = plant_targets(nt, npar, node_count, cfg.T_max)
+    target_next = torch.from_numpy(tn).cuda()
+    # The workload's caches are full at L; this one has room for a whole tree.
+    Lc = cfg.L + cfg.T_max + 1
+    kc = torch.zeros((cfg.B, cfg.Hkv, Lc, cfg.D), dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros_like(kc)
+    def call():
+        return adapld.accept_greedy(bufs.node_token, bufs.node_parent, bufs.node_depth, bufs.node_count,
+                                    bufs.tree_mask, target_next, lens, k_tree=s["k_tree"], v_tree=s["v_tree"],
+                                    k_ctx=kc, v_ctx=vc)
+    out = call()
+    torch.cuda.synchronize()
+    # One call costs the host more than the kernel takes, so a short spin
+    # kernel holds the stream while all calls are enqueued; the events then
+    # bracket the calls running back to back on the GPU.
+    n = max(steps, 20)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(int(n * 100e3))
+    e0.record(stream)
+    for _ in range(n):
+        out = call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / n * 1e3
+    kept = out[0].cpu().numpy()
+    nw = (cfg.T_max + 63) // 64
+    row = cfg.Hkv * cfg.D * 2   # bytes of one node's K (or V) row over all kv heads
+    n_copy = np.minimum(kept, Lc - np.clip(lens_np, 0, cfg.L))
+    byts = int(sum(12 * T + 8 * nw * T + 4 * (T + 1) + 8 for T in node_count)
+               + sum(4 + 4 * n + 4 * (n + 1) for n in kept) + int(n_copy.sum()) * row * 4)
+    del kc, vc
+    return {"kernel": "accept_greedy", "us": us, "algorithmic_bytes": byts,
+            "achieved_GBs": byts / (us * 1e-6) / 1e9, "kept_nodes_mean": float(kept.mean()),
+            "note": "after the step, not part of it; back-to-back calls; latency bound"}
+
+
 def measure(adapld, cfg, name, make_inputs, args):
     import torch
     log(f"[bench] generating {name}")
@@ -257,6 +325,8 @@ def measure(adapld, cfg, name, make_inputs, args):
         graph_us = g0.elapsed_time(g1) / steps * 1e3
         del graphs
 
+    acc = measure_accept(adapld, cfg, bufs, sets[0], x["lens"], lens, node_count, steps, stream)
+
     work = algorithmic_work(cfg, x["lens"], cand_count, node_count, node_depth)
     total_b, ver_b = work["total"], work["verify"]
     step_gbs = total_b / (step_ms * 1e-3) / 1e9
@@ -292,6 +362,7 @@ def measure(adapld, cfg, name, make_inputs, args):
         "roofline": {"kernel": "tree_verify_attn", "bound": "hbm", "achieved": ver_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": ver_gbs / HBM_PEAK_GBS, "traffic": verify_traffic(name),
                      "algorithmic_bytes_per_launch": ver_b, "launch_us": ver_ms * 1e3},
+        "accept": acc,
     }
     del sets, bufs
     torch.cuda.empty_cache()

@@ -59,13 +59,26 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_greedy_kernel(const Acc
   const int32_t* __restrict__ next = a.target_next + (size_t)b * (T_max + 1);
 
   // Match bit of node u: its token against the target's token after its parent.
+  // Every field of the node, its mask row included, is loaded at once and
+  // before node_count is known (rows below T_max are in bounds), so the loads
+  // share one memory round trip.
   bool match = false;
   int depth = 0;
-  if (u < T) {
+  uint64_t myrow[kMaskWordsMax];
+#pragma unroll
+  for (int w = 0; w < kMaskWordsMax; ++w)
+    myrow[w] = (u < T_max && w < nw) ? a.tree_mask[(nb + u) * nw + w] : 0ull;
+  if (u < T_max) {
     const int p = a.node_parent[nb + u];
+    const int tok = a.node_token[nb + u];
+    const int dep = a.node_depth[nb + u];
     const int want = p < 0 ? next[0] : (p < T_max ? next[1 + p] : INT32_MIN);
-    match = a.node_token[nb + u] == want;
-    depth = min(max(a.node_depth[nb + u], 0), T_max - 1);
+    match = u < T && tok == want;
+    depth = min(max(dep, 0), T_max - 1);
+  }
+  if (u >= T) {
+#pragma unroll
+    for (int w = 0; w < kMaskWordsMax; ++w) myrow[w] = 0ull;
   }
   if (u < ADAPLD_MAX_TREE_NODES) s_path[u] = -1;
   const uint64_t bits = __ballot(match);
@@ -76,9 +89,9 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_greedy_kernel(const Acc
   // then the lower node index.
   int key = -1;
   if (u < T) {
-    const uint64_t* __restrict__ row = a.tree_mask + (nb + u) * nw;
     bool ok = true;
-    for (int w = 0; w < nw; ++w) ok &= (row[w] & ~s_match[w]) == 0;
+#pragma unroll
+    for (int w = 0; w < kMaskWordsMax; ++w) ok &= w >= nw || (myrow[w] & ~s_match[w]) == 0;
     if (ok) key = (depth << 9) | (ADAPLD_MAX_TREE_NODES - 1 - u);
   }
   key = wave_max_i32(key);
@@ -89,10 +102,14 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_greedy_kernel(const Acc
   for (int w = 0; w < kAcceptThreads / kWave; ++w) best_key = max(best_key, s_best[w]);
   const int best = best_key < 0 ? -1 : ADAPLD_MAX_TREE_NODES - 1 - (best_key & 511);
 
-  // The path: the best node's ancestor-or-self row, placed by depth.
+  // The path: the best node's ancestor-or-self row (handed over by its
+  // thread), placed by depth.
   int n_acc = 0;
   if (best >= 0) {
-    if (u < nw) s_row[u] = a.tree_mask[(nb + best) * nw + u];
+    if (u == best) {
+#pragma unroll
+      for (int w = 0; w < kMaskWordsMax; ++w) s_row[w] = myrow[w];
+    }
     __syncthreads();
     for (int w = 0; w < nw; ++w) n_acc += __popcll(s_row[w]);
     if (u < T && ((s_row[u >> 6] >> (u & 63)) & 1ull) && depth < n_acc) s_path[depth] = u;
