@@ -206,28 +206,58 @@ __global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const Sc
     if (cb >= 0 && lane < a.k) a.ws_keys[((size_t)cb * a.lists + list) * a.k + lane] = mine;
     mine = 0;
   };
-  auto enter = [&](int g) {
+  auto query_of = [&](int b) {
+    return a.query ? a.query + (size_t)b * d : a.bank + ((size_t)b * a.L_stride + max(s_len[b] - 1, 0)) * d;
+  };
+  auto begin_segment = [&](int g) {
     flush();
     cb = seq_of(g);
     c_end = s_start[cb + 1];
     list = w - wave_of_row(s_start[cb], rows_total);
-    const int L = s_len[cb];
-    const uint16_t* qptr =
-        a.query ? a.query + (size_t)cb * d : a.bank + ((size_t)cb * a.L_stride + max(L - 1, 0)) * d;
+  };
+  auto set_norm = [&]() {
     float qn = 0.f;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) qn = dot8_bf16(qv[it], qv[it], qn);
+    qnorm = sqrtf(wave_sum_dpp(qn));
+  };
+  // A later segment (a range crossing into the next sequence) loads its query
+  // directly; the compiler's wait for it also drains the ring, which happens
+  // at most a few times per wave.
+  auto enter = [&](int g) {
+    begin_segment(g);
+    const uint16_t* qptr = query_of(cb);
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
       const int e = (it * kWave + lane) * 8;
       qv[it] = e < d ? *reinterpret_cast<const uint4*>(qptr + e) : make_uint4(0, 0, 0, 0);
-      qn = dot8_bf16(qv[it], qv[it], qn);
     }
-    qnorm = sqrtf(wave_sum_dpp(qn));
+    set_norm();
   };
 
-  // The first rows go out before the query is fetched, so the two latencies overlap.
+  // The first segment's query goes into the ring's last slot by direct loads,
+  // ahead of the first R-1 rows, so waiting for it leaves those rows in
+  // flight; row R-1 takes the slot once the query is in registers.
   int gp = g0;
-  for (; gp < g1 && gp - g0 < R; ++gp) issue(gp);
-  enter(g0);
+  {
+    const uint16_t* qptr = query_of(seq_of(g0));
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int e = (it * kWave + lane) * 8;
+      dma16(qptr + (e < d ? e : 0), ring + (R - 1) * kSlotBytes + it * 1024);
+    }
+  }
+  for (; gp < g1 && gp - g0 < R - 1; ++gp) issue(gp);
+  wait_rows<NIT, R>(gp - g0);
+  begin_segment(g0);
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int e = (it * kWave + lane) * 8;
+    const u32x4_t raw = ring_p[((R - 1) * kSlotBytes + it * 1024) / 16 + lane];
+    qv[it] = e < d ? make_uint4(raw[0], raw[1], raw[2], raw[3]) : make_uint4(0, 0, 0, 0);
+  }
+  set_norm();
+  if (gp < g1) issue(gp++);   // its wait for LDS reads covers the query's
   for (int g = g0; g < g1; ++g) {
     wait_rows<NIT, R>(min(gp - g - 1, R - 1));
     if (g >= c_end) enter(g);
