@@ -20,6 +20,10 @@ Four steps, per sequence, in the paper's order (Sec. 3.3 - 3.6, Algorithm 1):
                        each a copied span; an ancestor-or-self mask.
 ``tree_verify_attn``-- tree-masked attention over the KV cache (Sec. 3.6,
                        tree attention after Medusa), softmax in float64.
+``embedding_fallback`` -- the lexical/semantic backoff with the paper's own
+                       semantic signal (Sec. 3.3, Eqs. (4)-(5)): on a
+                       lexical miss, every earlier position whose token
+                       embedding has cosine >= tau with the last token's.
 ``accept_greedy``   -- greedy verification of the tree (Sec. 3.6 and the
                        speculative-decoding background of Appendix A: with
                        greedy decoding a draft token is kept when it equals
@@ -48,6 +52,11 @@ reproduced workload differs from its text):
   cache and is not a query row);
 * verification keys for node u are all context keys 0..L-1 followed by the
   tree keys of u's ancestors-or-self in ascending node order;
+* the token-embedding fallback scores positions j in [0, L-2] (the paper's
+  1 <= j < |M|, 1-based) by cos(e[M_j], e[M_{L-1}]) (a zero norm gives 0),
+  keeps those >= tau in ascending order, and is used only when the lexical
+  set is empty (then kind SEM if anything is kept, else NONE); the selection
+  among the kept positions is the hidden-state rerank of Sec. 3.4;
 * greedy acceptance takes the target's greedy token after the context (the
   root) and after every node as given (no model here); node u is accepted
   when its token equals the target's token after its parent and every
@@ -159,6 +168,27 @@ def semantic_topk(bank: np.ndarray, query, cand, k: int, tau=None):
         pos = [pos[i] for i in keep]
         sc = [sc[i] for i in keep]
     return (KIND_SEM if pos else KIND_NONE), pos, sc
+
+
+def embedding_fallback(tokens: np.ndarray, emb: np.ndarray, cand, tau: float):
+    """The lexical/semantic backoff rule with token-embedding similarity
+    (Sec. 3.3, Eqs. (4)-(5)).
+
+    tokens: (L,) ints; emb: (V, d) float64 token embeddings; cand: the lexical
+    candidate list.  A non-empty lexical list is the result (kind LEX).
+    Otherwise the result is every position j in [0, L-2] with
+    cos(emb[M_j], emb[M_{L-1}]) >= tau, ascending: kind SEM if non-empty,
+    else NONE.  Returns (kind, positions).
+    """
+    M = np.asarray(tokens)
+    L = int(M.shape[0])
+    if len(cand) > 0:
+        return KIND_LEX, [int(j) for j in cand]
+    if L < 2:
+        return KIND_NONE, []
+    s = cosine_rows(emb, M[:L - 1], emb[int(M[L - 1])])
+    C = [j for j in range(L - 1) if s[j] >= tau]
+    return (KIND_SEM if C else KIND_NONE), C
 
 
 # --------------------------------------------------------------------------

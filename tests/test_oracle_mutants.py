@@ -13,7 +13,8 @@ from concurrent.futures import ThreadPoolExecutor
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle_lexical.py", "tests/test_oracle_semantic.py",
-        "tests/test_oracle_tree.py", "tests/test_oracle_verify.py", "tests/test_oracle_accept.py"]
+        "tests/test_oracle_tree.py", "tests/test_oracle_verify.py", "tests/test_oracle_accept.py",
+        "tests/test_oracle_embedding.py"]
 
 MUTANTS = [
     ("js = np.arange(n - 1, L - 1)", "js = np.arange(n - 1, L)"),              # anchor counts itself
@@ -40,6 +41,10 @@ MUTANTS = [
     ("    bonus = int(node_next[best]) if best is not None else int(root_next)", "    bonus = int(root_next)"),
     ("        chain.reverse()\n", ""),                                         # walks the path bottom-up
     ("        K[:, L + i] = kt_bits[u]", "        K[:, L + i] = kt_bits[i]"),  # rows by rank, not node
+    ("    C = [j for j in range(L - 1) if s[j] >= tau]", "    C = [j for j in range(L - 1) if s[j] > tau]"),
+    ("    s = cosine_rows(emb, M[:L - 1], emb[int(M[L - 1])])", "    s = cosine_rows(emb, M[:L - 1], emb[int(M[L - 2])])"),
+    ("        return KIND_LEX, [int(j) for j in cand]\n", "        pass\n"),   # semantic set despite a hit
+    ("    C = [j for j in range(L - 1) if s[j] >= tau]", "    C = [j for j in range(L - 2) if s[j] >= tau]"),
 ]
 
 
