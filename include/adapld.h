@@ -73,6 +73,7 @@ extern "C" {
 #define ADAPLD_OP_SEMANTIC_TOPK 2
 #define ADAPLD_OP_BUILD_DRAFT_TREE 3
 #define ADAPLD_OP_TREE_VERIFY_ATTN 4
+#define ADAPLD_OP_SEMANTIC_TOPK_EMBED 5
 
 /* Limits of this implementation (larger values return ADAPLD_ERR_UNSUPPORTED). */
 #define ADAPLD_MAX_NMAX 64
@@ -239,6 +240,40 @@ int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint
                             int L_stride, int T_max, int Hq, int Hkv, int D, float scale,
                             uint16_t* out, float* lse, void* ws, size_t ws_bytes,
                             hipStream_t stream);
+
+/*
+ * adapld_semantic_topk_embed -- the lexical/semantic backoff with the paper's
+ * own semantic signal (Sec. 3.3, Eqs. (4)-(5)) followed by the hidden-state
+ * rerank (Sec. 3.4, Eqs. (6)-(7)).  A drop-in alternative to
+ * adapld_semantic_topk: same candidate inputs, same outputs.
+ *
+ * For a sequence with a lexical hit (cand_count[b] > 0) the candidates are
+ * its lexical set.  Otherwise they are the positions j in [0, L-2] whose
+ * token embedding has cosine >= tau with the embedding of the last token
+ * (emb rows of tokens[b, j] and tokens[b, L-1]; a token id outside [0, V)
+ * has a zero embedding, cosine 0), in ascending order.  The candidates are
+ * then ranked by cos(bank[b, r], q) exactly as adapld_semantic_topk ranks a
+ * lexical set, and the first min(k, #candidates) are kept.
+ *   bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, topk_*:
+ *              as for adapld_semantic_topk (query NULL: bank row L-1)
+ *   tokens     int32 [B, L_stride], the context
+ *   emb        bf16 [V, d], the target model's token embeddings
+ *              (16-byte aligned; same d as the bank)
+ *   tau        the embedding threshold of Eq. (4); must be finite
+ *   kind       LEX on a lexical hit, SEM when the embedding set is
+ *              non-empty, NONE otherwise (topk_count 0: an autoregressive
+ *              step; no hidden state is scanned for it)
+ *   ws         adapld_workspace_bytes(ADAPLD_OP_SEMANTIC_TOPK_EMBED, B,
+ *              L_stride, d, k, ...) bytes, 16-byte aligned
+ * Errors: NULL_ARG; INVALID_ARG (B < 0, L_stride < 1, d < 8 or d % 8, k < 1,
+ * V < 1, tau not finite, misaligned pointers); UNSUPPORTED (d > 8192,
+ * k > 64, B > ADAPLD_MAX_SEMANTIC_BATCH); WORKSPACE_TOO_SMALL.
+ */
+int adapld_semantic_topk_embed(const uint16_t* bank, const uint16_t* query, const int32_t* tokens,
+                               const int32_t* lens, const int32_t* cand_pos, const int32_t* cand_count,
+                               const uint16_t* emb, int V, int B, int L_stride, int d, int k, float tau,
+                               int32_t* topk_pos, float* topk_score, int32_t* topk_count, int32_t* kind,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * adapld_accept_greedy -- greedy verification of the draft tree (Sec. 3.6:

@@ -7,5 +7,5 @@ fallback.
 """
 from .binding import (  # noqa: F401
     KIND_LEX, KIND_NONE, KIND_SEM, AdapldError, StepBuffers, accept_greedy, build_draft_tree, lexical_match,
-    load_library, semantic_topk, step, tree_verify_attn, verify_plan, workspace_bytes,
+    load_library, semantic_topk, semantic_topk_embed, step, tree_verify_attn, verify_plan, workspace_bytes,
 )

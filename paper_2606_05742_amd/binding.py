@@ -18,6 +18,7 @@ import torch
 
 KIND_NONE, KIND_LEX, KIND_SEM = 0, 1, 2
 OP_LEXICAL_MATCH, OP_SEMANTIC_TOPK, OP_BUILD_DRAFT_TREE, OP_TREE_VERIFY_ATTN = 1, 2, 3, 4
+OP_SEMANTIC_TOPK_EMBED = 5
 HEAD_DIM = 128
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadapld.so")
@@ -48,6 +49,8 @@ SIGNATURES = {
         ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_float,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "adapld_semantic_topk_embed": (ctypes.c_int, [ctypes.c_void_p] * 7 + [ctypes.c_int] * 5 + [ctypes.c_float]
+                                   + [ctypes.c_void_p] * 5 + [ctypes.c_size_t, ctypes.c_void_p]),
     "adapld_build_draft_tree": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -168,6 +171,33 @@ def semantic_topk(bank, lens, cand_pos, cand_count, k, *, tau=None, query=None, 
         _ptr(topk_count, "topk_count", (torch.int32,), (B,)), _ptr(kind, "kind", (torch.int32,), (B,)),
         _ptr(ws, "ws", (torch.uint8,)), ws.numel(), _stream(stream))
     _check(st, "adapld_semantic_topk")
+    return topk_pos, topk_score, topk_count, kind
+
+
+def semantic_topk_embed(bank, tokens, lens, cand_pos, cand_count, emb, k, tau, *, query=None, topk_pos=None,
+                        topk_score=None, topk_count=None, kind=None, ws=None, stream=None):
+    """Backoff with the token-embedding fallback, then the hidden-state
+    rerank; returns (topk_pos, topk_score, topk_count, kind)."""
+    lib = load_library()
+    B, L_stride, d = bank.shape
+    V = emb.shape[0]
+    dev = bank.device
+    topk_pos = torch.empty((B, k), dtype=torch.int32, device=dev) if topk_pos is None else topk_pos
+    topk_score = torch.empty((B, k), dtype=torch.float32, device=dev) if topk_score is None else topk_score
+    topk_count = _i32(B, dev) if topk_count is None else topk_count
+    kind = _i32(B, dev) if kind is None else kind
+    need = workspace_bytes(OP_SEMANTIC_TOPK_EMBED, B, L_stride, d, k)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    st = lib.adapld_semantic_topk_embed(
+        _ptr(bank, "bank", _BF16_DTYPES), _ptr(query, "query", _BF16_DTYPES, (B, d), nullable=True),
+        _ptr(tokens, "tokens", (torch.int32,), (B, L_stride)), _ptr(lens, "lens", (torch.int32,), (B,)),
+        _ptr(cand_pos, "cand_pos", (torch.int32,), (B, L_stride)), _ptr(cand_count, "cand_count", (torch.int32,), (B,)),
+        _ptr(emb, "emb", _BF16_DTYPES, (V, d)), V, B, L_stride, d, k, float(tau),
+        _ptr(topk_pos, "topk_pos", (torch.int32,), (B, k)), _ptr(topk_score, "topk_score", (torch.float32,), (B, k)),
+        _ptr(topk_count, "topk_count", (torch.int32,), (B,)), _ptr(kind, "kind", (torch.int32,), (B,)),
+        _ptr(ws, "ws", (torch.uint8,)), ws.numel(), _stream(stream))
+    _check(st, "adapld_semantic_topk_embed")
     return topk_pos, topk_score, topk_count, kind
 
 

@@ -23,6 +23,9 @@ size_t semantic_ws(int B, int L_stride, int k) {
   return (size_t)B * adapld::scan_lists(L_stride) * k * sizeof(uint64_t);
 }
 
+// The embedding fallback's own part (16-byte aligned), then the scan's lists.
+size_t embed_head_ws(int B, int L_stride) { return (adapld::embed_ws_bytes(B, L_stride) + 15) / 16 * 16; }
+
 }  // namespace
 
 extern "C" {
@@ -52,6 +55,9 @@ size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_m
     case ADAPLD_OP_SEMANTIC_TOPK:
       if (k < 1 || k > ADAPLD_MAX_K) return 0;
       return semantic_ws(B, L_stride, k);
+    case ADAPLD_OP_SEMANTIC_TOPK_EMBED:
+      if (k < 1 || k > ADAPLD_MAX_K) return 0;
+      return embed_head_ws(B, L_stride) + semantic_ws(B, L_stride, k);
     case ADAPLD_OP_TREE_VERIFY_ATTN: {
       if (T_max < 1 || T_max > ADAPLD_MAX_TREE_NODES || Hq < 1 || Hkv < 1 || Hq % Hkv) return 0;
       const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
@@ -107,6 +113,35 @@ int adapld_semantic_topk(const uint16_t* bank, const uint16_t* query, const int3
   return hip_status(adapld::launch_semantic_topk(bank, query, lens, cand_pos, cand_count, B,
                                                  L_stride, d, k, tau, topk_pos, topk_score,
                                                  topk_count, kind, static_cast<uint64_t*>(ws),
+                                                 nullptr, 0, stream));
+}
+
+int adapld_semantic_topk_embed(const uint16_t* bank, const uint16_t* query, const int32_t* tokens,
+                               const int32_t* lens, const int32_t* cand_pos, const int32_t* cand_count,
+                               const uint16_t* emb, int V, int B, int L_stride, int d, int k, float tau,
+                               int32_t* topk_pos, float* topk_score, int32_t* topk_count, int32_t* kind,
+                               void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!bank || !tokens || !lens || !cand_pos || !cand_count || !emb || !topk_pos || !topk_score ||
+      !topk_count || !kind || !ws)
+    return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || d < 8 || d % 8 != 0 || k < 1 || V < 1 || !std::isfinite(tau))
+    return ADAPLD_ERR_INVALID_ARG;
+  if (d > ADAPLD_MAX_HIDDEN || k > ADAPLD_MAX_K || B > ADAPLD_MAX_SEMANTIC_BATCH ||
+      (int64_t)B * L_stride > INT32_MAX)
+    return ADAPLD_ERR_UNSUPPORTED;
+  if (misaligned16(bank) || (query && misaligned16(query)) || misaligned16(emb) || misaligned16(ws))
+    return ADAPLD_ERR_INVALID_ARG;
+  const size_t head = embed_head_ws(B, L_stride);
+  if (ws_bytes < head + semantic_ws(B, L_stride, k)) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  int32_t *cands = nullptr, *counts = nullptr, *kinds = nullptr;
+  hipError_t e = adapld::launch_embedding_fallback(tokens, lens, cand_pos, cand_count, emb, V, B, L_stride, d,
+                                                   tau, ws, &cands, &counts, &kinds, stream);
+  if (e != hipSuccess) return hip_status(e);
+  uint64_t* keys = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + head);
+  return hip_status(adapld::launch_semantic_topk(bank, query, lens, cands, counts, B, L_stride, d, k, NAN,
+                                                 topk_pos, topk_score, topk_count, kind, keys, kinds, 1,
                                                  stream));
 }
 

@@ -55,7 +55,8 @@ hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, con
                                 const int32_t* cand_pos, const int32_t* cand_count, int B,
                                 int L_stride, int d, int k, float tau, int32_t* topk_pos,
                                 float* topk_score, int32_t* topk_count, int32_t* kind,
-                                uint64_t* ws_keys, hipStream_t stream);
+                                uint64_t* ws_keys, const int32_t* cand_kind, int rerank_only,
+                                hipStream_t stream);
 
 hipError_t launch_build_draft_tree(const int32_t* tokens, const int32_t* lens,
                                    const int32_t* topk_pos, const int32_t* topk_count,
@@ -70,6 +71,15 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
                                    const uint64_t* tree_mask, int B, int L_stride, int T_max,
                                    int Hq, int Hkv, float scale, uint16_t* out, float* lse,
                                    void* ws, const VerifyPlan& plan, hipStream_t stream);
+
+size_t embed_ws_bytes(int B, int L_stride);
+
+// Writes the lexical/embedding candidate set, its size and its kind into ws
+// and returns pointers to them.
+hipError_t launch_embedding_fallback(const int32_t* tokens, const int32_t* lens, const int32_t* cand_pos,
+                                     const int32_t* cand_count, const uint16_t* emb, int V, int B,
+                                     int L_stride, int d, float tau, void* ws, int32_t** cands,
+                                     int32_t** counts, int32_t** kinds, hipStream_t stream);
 
 hipError_t launch_accept_greedy(const int32_t* node_token, const int32_t* node_parent,
                                 const int32_t* node_depth, const int32_t* node_count,

@@ -1,0 +1,225 @@
+// The paper's own semantic fallback (Sec. 3.3, Eqs. (4)-(5)): when the lexical
+// set of a sequence is empty, its candidates are the earlier positions j in
+// [0, L-2] whose token embedding has cosine >= tau with the embedding of the
+// last token; the hidden-state rerank of Sec. 3.4 then ranks them.
+//
+// flags kernel: workgroups of 4 waves tile the positions of every sequence
+// whose lexical set is empty, 16 positions per wave.  A wave holds the anchor
+// embedding in registers, reads the 16 token ids with one load, gathers the
+// embedding row of each position's token (two rows in flight, 16-byte
+// coalesced loads; rows of frequent tokens come from L2 and the last-level
+// cache, so HBM sees roughly one read per distinct token), reduces the dot
+// product and the squared norm with the same fixed DPP butterfly as the
+// hidden-state scan, and writes one flag byte per position.
+//
+// compact kernel: one workgroup per sequence writes the candidate set in
+// ascending order (a non-empty lexical set is copied through), its size and
+// its kind, with per-thread runs of 32 flags and a wave + workgroup scan of
+// the run counts (as the lexical kernel orders its hits).
+//
+// The rerank is the hidden-state scan and merge kernels in rerank-only mode.
+#include <cmath>
+
+#include "adapld_internal.h"
+#include "device_utils.h"
+
+namespace adapld {
+namespace {
+
+constexpr int kFlagWaves = 4;
+constexpr int kPosPerWave = 16;
+constexpr int kPosPerWg = kFlagWaves * kPosPerWave;
+constexpr int kCompactThreads = 1024;
+constexpr int kCompactRun = 32;                                 // flags per thread per piece
+constexpr int kCompactPiece = kCompactThreads * kCompactRun;
+
+struct EmbedArgs {
+  const int32_t* tokens;
+  const int32_t* lens;
+  const int32_t* cand_pos;
+  const int32_t* cand_count;
+  const uint16_t* emb;
+  int V, B, L_stride, d, flag_stride;
+  float tau;
+  uint8_t* flags;       // [B][flag_stride]
+  int32_t* out_pos;     // [B][L_stride]
+  int32_t* out_count;   // [B]
+  int32_t* out_kind;    // [B]
+};
+
+// cos(emb[t], anchor) >= tau for one gathered row; a token outside [0, V) has
+// a zero embedding (cosine 0).
+template <int NIT>
+__global__ __launch_bounds__(kFlagWaves * kWave) void embed_flags_kernel(const EmbedArgs a) {
+  const int b = blockIdx.y;
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  if (a.cand_count[b] > 0) return;   // a lexical hit needs no flags
+  const int L = min(max(a.lens[b], 0), a.L_stride);
+  const int J = L - 1;               // positions [0, J)
+  const int j0 = blockIdx.x * kPosPerWg + wave * kPosPerWave;
+  if (j0 >= J) return;
+  const int32_t* __restrict__ M = a.tokens + (size_t)b * a.L_stride;
+  const int d = a.d;
+
+  const int at = M[L - 1];
+  const bool a_ok = at >= 0 && at < a.V;
+  const int my_tok = lane < kPosPerWave && j0 + lane < J ? M[j0 + lane] : -1;
+  uint4 qv[NIT];
+  float qn = 0.f;
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int e = (it * kWave + lane) * 8;
+    qv[it] = a_ok && e < d ? *reinterpret_cast<const uint4*>(a.emb + (size_t)at * d + e) : make_uint4(0, 0, 0, 0);
+    qn = dot8_bf16(qv[it], qv[it], qn);
+  }
+  const float qnorm = sqrtf(wave_sum_dpp(qn));
+
+  auto score = [&](const uint4 (&rv)[NIT]) {
+    float dot = 0.f, nn = 0.f;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      dot = dot8_bf16(rv[it], qv[it], dot);
+      nn = dot8_bf16(rv[it], rv[it], nn);
+    }
+    dot = wave_sum_dpp(dot);
+    nn = wave_sum_dpp(nn);
+    const float den = sqrtf(nn) * qnorm;
+    return den > 0.f ? dot / den : 0.f;
+  };
+  auto load_row = [&](int t, uint4 (&rv)[NIT]) {
+    const bool ok = t >= 0 && t < a.V;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int e = (it * kWave + lane) * 8;
+      rv[it] = ok && e < d ? *reinterpret_cast<const uint4*>(a.emb + (size_t)t * d + e) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  uint8_t* __restrict__ fl = a.flags + (size_t)b * a.flag_stride;
+  const int n = min(kPosPerWave, J - j0);
+  for (int i = 0; i < n; i += 2) {
+    uint4 r0[NIT], r1[NIT];
+    const int t0 = __builtin_amdgcn_readlane(my_tok, i);
+    const int t1 = i + 1 < n ? __builtin_amdgcn_readlane(my_tok, i + 1) : -1;
+    load_row(t0, r0);
+    load_row(t1, r1);
+    const float s0 = score(r0);
+    const float s1 = score(r1);
+    if (lane == 0) {
+      fl[j0 + i] = s0 >= a.tau ? 1 : 0;
+      if (i + 1 < n) fl[j0 + i + 1] = s1 >= a.tau ? 1 : 0;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kCompactThreads) void embed_compact_kernel(const EmbedArgs a) {
+  __shared__ int s_red[kCompactThreads / kWave];
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid / kWave;
+  const int cc = min(max(a.cand_count[b], 0), a.L_stride);
+  int32_t* __restrict__ out = a.out_pos + (size_t)b * a.L_stride;
+  if (cc > 0) {   // the backoff rule: a lexical set is the result
+    const int32_t* __restrict__ in = a.cand_pos + (size_t)b * a.L_stride;
+    for (int i = tid; i < cc; i += kCompactThreads) out[i] = in[i];
+    if (tid == 0) {
+      a.out_count[b] = cc;
+      a.out_kind[b] = ADAPLD_KIND_LEX;
+    }
+    return;
+  }
+  const int L = min(max(a.lens[b], 0), a.L_stride);
+  const int J = max(L - 1, 0);
+  const uint8_t* __restrict__ fl = a.flags + (size_t)b * a.flag_stride;
+  int total = 0;
+  for (int p0 = 0; p0 < J; p0 += kCompactPiece) {
+    // Thread tid owns positions [q0, q0 + 32) of this piece (16-byte aligned).
+    const int q0 = p0 + tid * kCompactRun;
+    uint32_t bits = 0;
+    if (q0 < J) {
+      const uint4 f0 = *reinterpret_cast<const uint4*>(fl + q0);
+      const uint4 f1 = *reinterpret_cast<const uint4*>(fl + q0 + 16);
+      const uint32_t w[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+#pragma unroll
+      for (int e = 0; e < kCompactRun; ++e)
+        if (((w[e >> 2] >> (8 * (e & 3))) & 0xffu) != 0u && q0 + e < J) bits |= 1u << e;
+    }
+    const int cnt = __popc(bits);
+    const int incl = wave_incl_scan_i32(cnt);
+    __syncthreads();   // earlier reads of s_red are done
+    if (lane == kWave - 1) s_red[wave] = incl;
+    __syncthreads();
+    int before = 0, piece = 0;
+#pragma unroll
+    for (int w = 0; w < kCompactThreads / kWave; ++w) {
+      const int c = s_red[w];
+      before += w < wave ? c : 0;
+      piece += c;
+    }
+    int slot = total + before + incl - cnt;
+    while (bits) {
+      const int e = __builtin_ctz(bits);
+      bits &= bits - 1;
+      out[slot++] = q0 + e;
+    }
+    total += piece;
+  }
+  if (tid == 0) {
+    a.out_count[b] = total;
+    a.out_kind[b] = total > 0 ? ADAPLD_KIND_SEM : ADAPLD_KIND_NONE;
+  }
+}
+
+template <int NIT>
+void launch_flags(const EmbedArgs& a, int B, hipStream_t stream) {
+  const dim3 grid((a.L_stride + kPosPerWg - 1) / kPosPerWg, B);
+  hipLaunchKernelGGL(embed_flags_kernel<NIT>, grid, dim3(kFlagWaves * kWave), 0, stream, a);
+}
+
+}  // namespace
+
+size_t embed_ws_bytes(int B, int L_stride) {
+  // flags (rows padded to whole 32-flag runs of the compaction, 16-byte
+  // aligned), then the candidate list, its size and its kind
+  const size_t stride = ((size_t)L_stride + kCompactRun - 1) / kCompactRun * kCompactRun;
+  return (size_t)B * stride + (size_t)B * L_stride * 4 + (size_t)B * 8;
+}
+
+hipError_t launch_embedding_fallback(const int32_t* tokens, const int32_t* lens, const int32_t* cand_pos,
+                                     const int32_t* cand_count, const uint16_t* emb, int V, int B,
+                                     int L_stride, int d, float tau, void* ws, int32_t** cands,
+                                     int32_t** counts, int32_t** kinds, hipStream_t stream) {
+  const size_t stride = ((size_t)L_stride + kCompactRun - 1) / kCompactRun * kCompactRun;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  EmbedArgs a{};
+  a.tokens = tokens; a.lens = lens; a.cand_pos = cand_pos; a.cand_count = cand_count; a.emb = emb;
+  a.V = V; a.B = B; a.L_stride = L_stride; a.d = d; a.flag_stride = (int)stride; a.tau = tau;
+  a.flags = base;
+  a.out_pos = reinterpret_cast<int32_t*>(base + (size_t)B * stride);
+  a.out_count = a.out_pos + (size_t)B * L_stride;
+  a.out_kind = a.out_count + B;
+  *cands = a.out_pos;
+  *counts = a.out_count;
+  *kinds = a.out_kind;
+  const int nit = (d + 8 * kWave - 1) / (8 * kWave);
+  switch (nit) {
+#define ADAPLD_FLAGS_CASE(n) \
+  case n:                    \
+    launch_flags<n>(a, B, stream); \
+    break;
+    ADAPLD_FLAGS_CASE(1) ADAPLD_FLAGS_CASE(2) ADAPLD_FLAGS_CASE(3) ADAPLD_FLAGS_CASE(4)
+    ADAPLD_FLAGS_CASE(5) ADAPLD_FLAGS_CASE(6) ADAPLD_FLAGS_CASE(7) ADAPLD_FLAGS_CASE(8)
+    ADAPLD_FLAGS_CASE(9) ADAPLD_FLAGS_CASE(10) ADAPLD_FLAGS_CASE(11) ADAPLD_FLAGS_CASE(12)
+    ADAPLD_FLAGS_CASE(13) ADAPLD_FLAGS_CASE(14) ADAPLD_FLAGS_CASE(15) ADAPLD_FLAGS_CASE(16)
+#undef ADAPLD_FLAGS_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(embed_compact_kernel, dim3(B), dim3(kCompactThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace adapld

@@ -32,18 +32,8 @@ namespace {
 constexpr int kScanThreads = kScanWaves * kWave;
 constexpr int kScanRingBytes = 32768;   // LDS ring per wave
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) u32x4_t lds_u32x4;
-
-// acc + sum of the 8 products of two 8-element bf16 vectors, fp32 accumulation.
-__device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b, float acc) {
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.x), __builtin_bit_cast(bf16x2_t, b.x), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.y), __builtin_bit_cast(bf16x2_t, b.y), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.z), __builtin_bit_cast(bf16x2_t, b.z), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.w), __builtin_bit_cast(bf16x2_t, b.w), acc, false);
-  return acc;
-}
 
 // Rows held by a wave's ring: a row occupies NIT KiB (one KiB per 16-byte
 // load of the whole wave); 2 to 8 rows, at most 32 KiB.
@@ -60,12 +50,14 @@ struct ScanArgs {
   const int32_t* cand_count;
   int B, L_stride, d, k, lists;   // lists = segment-list slots per sequence
   uint64_t* ws_keys;              // [B][lists][k]
+  const int32_t* cand_kind;       // kind of a non-empty candidate set (NULL: LEX)
+  int rerank_only;                // 1: an empty candidate set scores nothing (kind NONE)
 };
 
 __device__ __forceinline__ void seq_rows(const ScanArgs& a, int b, int& L, int& cc, int& nrows) {
   L = min(max(a.lens[b], 0), a.L_stride);
   cc = min(max(a.cand_count[b], 0), a.L_stride);
-  nrows = cc > 0 ? cc : max(L - 1, 0);
+  nrows = cc > 0 ? cc : (a.rerank_only ? 0 : max(L - 1, 0));
 }
 
 // Rows are split over W = min(kScanWaveSlots, total) waves, wave w taking
@@ -392,7 +384,8 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
   }
   if (lane == 0) {
     topk_count[b] = count;
-    kind[b] = cc > 0 ? ADAPLD_KIND_LEX : (count > 0 ? ADAPLD_KIND_SEM : ADAPLD_KIND_NONE);
+    kind[b] = cc > 0 ? (a.cand_kind ? a.cand_kind[b] : ADAPLD_KIND_LEX)
+                     : (count > 0 ? ADAPLD_KIND_SEM : ADAPLD_KIND_NONE);
   }
 }
 
@@ -408,8 +401,10 @@ hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, con
                                 const int32_t* cand_pos, const int32_t* cand_count, int B,
                                 int L_stride, int d, int k, float tau, int32_t* topk_pos,
                                 float* topk_score, int32_t* topk_count, int32_t* kind,
-                                uint64_t* ws_keys, hipStream_t stream) {
-  ScanArgs a{bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, scan_lists(L_stride), ws_keys};
+                                uint64_t* ws_keys, const int32_t* cand_kind, int rerank_only,
+                                hipStream_t stream) {
+  ScanArgs a{bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, scan_lists(L_stride), ws_keys,
+             cand_kind, rerank_only};
   const int nit = (d + 8 * kWave - 1) / (8 * kWave);
   switch (nit) {
 #define ADAPLD_SCAN_CASE(n) \

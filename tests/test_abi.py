@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     for n in names:
         assert hasattr(lib, n), n
         assert n in binding.SIGNATURES, n
@@ -74,6 +74,28 @@ def test_verify_plan(lib):
         p = binding.verify_plan(B, L, T, Hq, Hkv)
         seen.add((p["kh"], p["nsplit"] > 1))
     assert seen == {(1, False), (1, True), (2, False), (2, True)}
+
+
+def test_embed_validation(lib):
+    f = lib.adapld_semantic_topk_embed
+    nan = float("nan")
+    args = lambda **kw: [kw.get(n, v) for n, v in (  # noqa: E731
+        ("bank", P), ("query", N), ("tokens", P), ("lens", P), ("cand_pos", P), ("cand_count", P), ("emb", P),
+        ("V", 100), ("B", 2), ("L_stride", 64), ("d", 128), ("k", 8), ("tau", 0.5),
+        ("pos", P), ("score", P), ("count", P), ("kind", P), ("ws", P), ("ws_bytes", 1 << 30), ("stream", N))]
+    assert f(*args(B=0)) == OK
+    assert f(*args(B=-1)) == INVALID
+    assert f(*args(emb=N)) == NULL
+    assert f(*args(tokens=N)) == NULL
+    assert f(*args(ws=N)) == NULL
+    assert f(*args(tau=nan)) == INVALID                 # the threshold is required
+    assert f(*args(V=0)) == INVALID
+    assert f(*args(d=12)) == INVALID
+    assert f(*args(k=65)) == UNSUPPORTED
+    assert f(*args(emb=ctypes.c_void_p(0x10008))) == INVALID
+    need = lib.adapld_workspace_bytes(5, 2, 64, 128, 8, 0, 0, 0, 0)
+    assert need >= lib.adapld_workspace_bytes(2, 2, 64, 128, 8, 0, 0, 0, 0) + 2 * 64 * 5
+    assert f(*args(ws_bytes=need - 1)) == WS_SMALL
 
 
 def test_accept_validation(lib):

@@ -1,0 +1,124 @@
+"""GPU parity of adapld_semantic_topk_embed (the token-embedding fallback of
+Sec. 3.3, Eqs. (4)-(5), then the hidden-state rerank of Sec. 3.4) against
+the oracle: the kind of every sequence, and the ranked list of the
+candidates the oracle's fallback keeps."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_05742_amd as adapld
+from paper_2606_05742_amd.synth import f32_to_bf16_bits, make_inputs, small_config
+from parity_helpers import check_ranked, dev_bf16, dev_i32
+
+pytestmark = pytest.mark.gpu
+
+
+def emb_table(V, d, clusters, seed, zero_rows=()):
+    """Token embeddings in clusters (tokens t and t' of the same cluster
+    t % clusters have a high cosine), bf16 bits."""
+    rng = np.random.default_rng(seed)
+    centers = rng.standard_normal((clusters, d))
+    E = centers[np.arange(V) % clusters] + 0.35 * rng.standard_normal((V, d))
+    for r in zero_rows:
+        E[r] = 0.0
+    return f32_to_bf16_bits(E.astype(np.float32))
+
+
+def margin_ok(E, tokens, lens, tau, margin=1e-3):
+    for b in range(tokens.shape[0]):
+        L = int(lens[b])
+        if L < 2:
+            continue
+        s = oracle.cosine_rows(E, tokens[b, :L - 1], E[int(tokens[b, L - 1])])
+        if np.any(np.abs(s - tau) < margin):
+            return False
+    return True
+
+
+def run_and_check(cfg, x, E_bits, tau, k, ctx):
+    E = oracle.bf16_bits_to_f64(E_bits)
+    assert margin_ok(E, x["tokens"], x["lens"], tau), "pick another tau: a cosine sits on it"
+    tokens, lens = dev_i32(x["tokens"]), dev_i32(x["lens"])
+    cp, cc, mn = adapld.lexical_match(tokens, lens, cfg.n_max)
+    pos, sc, cnt, kind = adapld.semantic_topk_embed(dev_bf16(x["bank"]), tokens, lens, cp, cc, dev_bf16(E_bits),
+                                                    k, tau)
+    torch.cuda.synchronize()
+    pos, sc, cnt, kind = (t.cpu().numpy() for t in (pos, sc, cnt, kind))
+    kinds = []
+    for b in range(cfg.B):
+        L = int(x["lens"][b])
+        M = x["tokens"][b, :L]
+        _, C = oracle.lexical_match(M, cfg.n_max)
+        ekind, Cs = oracle.embedding_fallback(M, E, C, tau)
+        assert int(kind[b]) == ekind, (ctx, b, int(kind[b]), ekind)
+        kinds.append(ekind)
+        if ekind == oracle.KIND_NONE:
+            assert int(cnt[b]) == 0, (ctx, b)
+            continue
+        n = int(cnt[b])
+        check_ranked(oracle.bf16_bits_to_f64(x["bank"][b, :L]), None, Cs, k, None, oracle.KIND_LEX,
+                     [int(p) for p in pos[b, :n]], [float(s) for s in sc[b, :n]], f"{ctx} b={b}")
+    return kinds
+
+
+@pytest.mark.parametrize("L,d,k,tau", [(300, 256, 8, 0.5), (2100, 128, 64, 0.45), (700, 520, 16, 0.55)])
+def test_embedding_fallback(L, d, k, tau):
+    cfg = small_config(B=8, L=L, d=d, k=k, n_max=3, seed=140 + L % 97, V=60, forced_every=2)
+    x = make_inputs(cfg, with_verify=False)
+    E_bits = emb_table(cfg.V + 8, d, clusters=6, seed=L, zero_rows=(7,))   # ids reach V (c.17)
+    kinds = run_and_check(cfg, x, E_bits, tau, k, f"L={L}")
+    assert oracle.KIND_SEM in kinds and oracle.KIND_LEX in kinds, kinds
+
+
+def test_embedding_fallback_nothing_kept():
+    """tau above every cosine: each lexical miss is an autoregressive step."""
+    cfg = small_config(B=4, L=400, d=128, k=8, n_max=3, seed=151, V=60, forced_every=1)
+    x = make_inputs(cfg, with_verify=False)
+    E_bits = emb_table(cfg.V + 8, 128, clusters=6, seed=3)
+    kinds = run_and_check(cfg, x, E_bits, 1.01, 8, "tau>1")
+    assert set(kinds) <= {oracle.KIND_NONE, oracle.KIND_LEX} and oracle.KIND_NONE in kinds
+
+
+def test_embedding_fallback_two_pieces():
+    """A context longer than one compaction piece (32768 positions)."""
+    cfg = small_config(B=2, L=40000, d=64, k=16, n_max=3, seed=152, V=40, forced_every=1)
+    x = make_inputs(cfg, with_verify=False)
+    E_bits = emb_table(cfg.V + 8, 64, clusters=5, seed=9)
+    kinds = run_and_check(cfg, x, E_bits, 0.6, 16, "L=40000")
+    assert oracle.KIND_SEM in kinds
+
+
+def test_embedding_fallback_out_of_range_tokens():
+    """Token ids outside [0, V) have a zero embedding (cosine 0): kept for
+    tau <= 0, dropped for tau > 0."""
+    cfg = small_config(B=3, L=500, d=128, k=64, n_max=3, seed=153, V=50, forced_every=1)
+    x = make_inputs(cfg, with_verify=False)
+    V = cfg.V + 8   # table rows; generated ids reach cfg.V
+    rng = np.random.default_rng(4)
+    for b in range(cfg.B):
+        L = int(x["lens"][b])
+        idx = rng.choice(L - 1, size=12, replace=False)
+        x["tokens"][b, idx] = np.where(rng.random(12) < 0.5, -3, V + 7)
+    E_bits = emb_table(V, 128, clusters=5, seed=11)
+    # the oracle sees the same ids mapped to an extra zero row
+    E_ext = np.concatenate([E_bits, np.zeros((1, 128), dtype=np.uint16)])
+    xm = dict(x)
+    xm["tokens"] = np.where((x["tokens"] < 0) | (x["tokens"] >= V), V, x["tokens"])
+    for tau in (-0.2, 0.5):
+        E = oracle.bf16_bits_to_f64(E_ext)
+        assert margin_ok(E, xm["tokens"], x["lens"], tau)
+        tokens, lens = dev_i32(x["tokens"]), dev_i32(x["lens"])
+        cp, cc, mn = adapld.lexical_match(tokens, lens, cfg.n_max)
+        pos, sc, cnt, kind = adapld.semantic_topk_embed(dev_bf16(x["bank"]), tokens, lens, cp, cc, dev_bf16(E_bits),
+                                                        64, tau)
+        torch.cuda.synchronize()
+        cnt, kind, pos = cnt.cpu().numpy(), kind.cpu().numpy(), pos.cpu().numpy()
+        for b in range(cfg.B):
+            L = int(x["lens"][b])
+            # the lexical match runs on the original ids (they differ from every real id)
+            _, C = oracle.lexical_match(x["tokens"][b, :L], cfg.n_max)
+            ekind, Cs = oracle.embedding_fallback(xm["tokens"][b, :L], E, C, tau)
+            assert int(kind[b]) == ekind, (tau, b)
+            if ekind == oracle.KIND_SEM and len(Cs) <= 64:
+                assert sorted(int(p) for p in pos[b, :int(cnt[b])]) == sorted(Cs), (tau, b)
