@@ -234,6 +234,65 @@ def measure_accept(adapld, cfg, bufs, s, lens_np, lens, node_count, steps, strea
             "note": "after the step, not part of it; back-to-back calls; latency bound"}
 
 
+def measure_embed(adapld, cfg, bufs, s, tokens, lens, x, steps, stream):
+    """The paper's token-embedding fallback (adapld_semantic_topk_embed) next
+    to the hidden-state fallback (adapld_semantic_topk), each timed back to
+    back behind a spin kernel on the step's own lexical results.  The
+    embedding table is synthetic: V rows in 1024 clusters (rows of one cluster
+    have cosine about 0.9, others about 0), generated on the GPU from a fixed
+    seed; tau = 0.5 keeps the anchor's cluster."""
+    import torch
+    V, d = cfg.V + 8, cfg.d   # generated ids reach cfg.V
+    g = torch.Generator(device="cuda").manual_seed(1234)
+    centers = torch.randn((1024, d), generator=g, device="cuda")
+    emb = (centers[torch.arange(V, device="cuda") % 1024]
+           + 0.35 * torch.randn((V, d), generator=g, device="cuda")).to(torch.bfloat16)
+    del centers
+    tau = 0.5
+    n = max(steps, 20)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(int(n * 400e3))
+        e0.record(stream)
+        for _ in range(n):
+            out = fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e3, out
+
+    def hidden():
+        return adapld.semantic_topk(s["bank"], lens, bufs.cand_pos, bufs.cand_count, cfg.k)
+
+    def embed():
+        return adapld.semantic_topk_embed(s["bank"], tokens, lens, bufs.cand_pos, bufs.cand_count, emb, cfg.k, tau)
+
+    adapld.lexical_match(tokens, lens, cfg.n_max, cand_pos=bufs.cand_pos, cand_count=bufs.cand_count,
+                         match_n=bufs.match_n)
+    us_hidden, _ = timed(hidden)
+    us_embed, out = timed(embed)
+    kind = out[3].cpu().numpy()
+    cc = bufs.cand_count.cpu().numpy()
+    L = np.clip(x["lens"], 0, cfg.L)
+    miss = cc == 0
+    # algorithmic bytes: token ids and one embedding row per distinct token of
+    # every missed sequence, one flag byte written and read per position, the
+    # candidate list, then the rerank's bank rows and query
+    uniq = sum(len(np.unique(x["tokens"][b, :max(L[b] - 1, 0)])) + 1 for b in np.nonzero(miss)[0])
+    npos = int(sum(max(L[b] - 1, 0) for b in np.nonzero(miss)[0]))
+    ncand = int(out[2].cpu().numpy().sum())
+    byts = int(4 * npos + 2 * d * uniq + 2 * npos + 4 * npos + 2 * d * (ncand + cfg.B))
+    del emb
+    return {"call": "adapld_semantic_topk_embed", "us": us_embed, "hidden_state_fallback_us": us_hidden,
+            "algorithmic_bytes": byts, "tau": tau, "vocab": V,
+            "kinds": {"lex": int((kind == 1).sum()), "sem": int((kind == 2).sum()), "none": int((kind == 0).sum())},
+            "note": "the paper's token-embedding fallback in place of the hidden-state one, back-to-back calls; "
+                    "not part of the step"}
+
+
 def measure(adapld, cfg, name, make_inputs, args):
     import torch
     log(f"[bench] generating {name}")
@@ -326,6 +385,7 @@ def measure(adapld, cfg, name, make_inputs, args):
         del graphs
 
     acc = measure_accept(adapld, cfg, bufs, sets[0], x["lens"], lens, node_count, steps, stream)
+    emb = measure_embed(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
 
     work = algorithmic_work(cfg, x["lens"], cand_count, node_count, node_depth)
     total_b, ver_b = work["total"], work["verify"]
@@ -363,6 +423,7 @@ def measure(adapld, cfg, name, make_inputs, args):
                      "unit": "GB/s", "frac": ver_gbs / HBM_PEAK_GBS, "traffic": verify_traffic(name),
                      "algorithmic_bytes_per_launch": ver_b, "launch_us": ver_ms * 1e3},
         "accept": acc,
+        "embedding_fallback": emb,
     }
     del sets, bufs
     torch.cuda.empty_cache()
