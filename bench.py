@@ -30,8 +30,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "55cc72f9917459d76ea7e024f8e519ce8e7b921110f33a4cf8b72b2c3fe57a0c",
-    "fetch_kib": 268951.9,
+    "source_sha256": "6c500a7bda61215f08b61d0e42f27efaf31860353b734f543c470d415a101b05",
+    "fetch_kib": 269412.9,
     "write_kib": 5392.1,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
@@ -132,6 +132,8 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the acceptance and embedding-fallback timings after the step")
     ap.add_argument("--all-configs", action="store_true",
                     help="one JSON line per workload (the parity configurations), no CPU baseline")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -384,8 +386,10 @@ def measure(adapld, cfg, name, make_inputs, args):
         graph_us = g0.elapsed_time(g1) / steps * 1e3
         del graphs
 
-    acc = measure_accept(adapld, cfg, bufs, sets[0], x["lens"], lens, node_count, steps, stream)
-    emb = measure_embed(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
+    acc = emb = None
+    if not args.no_extras:
+        acc = measure_accept(adapld, cfg, bufs, sets[0], x["lens"], lens, node_count, steps, stream)
+        emb = measure_embed(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
 
     work = algorithmic_work(cfg, x["lens"], cand_count, node_count, node_depth)
     total_b, ver_b = work["total"], work["verify"]
