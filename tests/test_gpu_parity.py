@@ -318,3 +318,17 @@ def test_full_config(name):
                      [float(s) for s in g["topk_score"][b, :tc]], f"{name} b={b}")
         check_tree(x["tokens"][b, :L], int(g["kind"][b]), gpos, cfg.W, cfg.S, g, b, f"{name} b={b}")
     log(f"[{name}] kinds(sampled)={kinds} fallback={int((g['cand_count'] == 0).sum())}/{cfg.B}")
+
+
+def test_benchmark_workload_every_node():
+    """The benchmark's workload (b16_l8192_gqa32x8) in the launch configuration
+    bench.py times: every draft node of two sequences (a lexical hit and a
+    forced fallback) against the oracle's tree attention, not just sampled
+    nodes."""
+    cfg = CONFIGS["b16_l8192_gqa32x8"]
+    x = make_inputs(cfg)
+    g = run_step(cfg, upload(x))
+    hit = next(b for b in range(cfg.B) if not x["forced"][b] and int(g["cand_count"][b]) > 0)
+    forced = next(b for b in range(cfg.B) if x["forced"][b])
+    check_all(cfg, x, g, verify_nodes=None, seqs=[hit, forced], ctx="every node")
+    assert int(g["node_count"][hit]) > 1 and int(g["node_count"][forced]) > 1
