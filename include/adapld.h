@@ -13,6 +13,11 @@
  *                               (Sec. 3.5, Sec. 3.6)
  *   4. adapld_tree_verify_attn  tree-masked verify attention (Sec. 3.6)
  *
+ * Call 2 has a drop-in alternative with the paper's own semantic signal,
+ * token-embedding similarity (Sec. 3.3, Eq. (4)):
+ *
+ *   2'. adapld_semantic_topk_embed
+ *
  * and, once the target's greedy tokens for the verified tree are known,
  *
  *   5. adapld_accept_greedy     greedy acceptance of the tree and compaction
@@ -226,6 +231,7 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
  *   out        bf16 [B, T_max, Hq, D]  (out) rows u >= T are not written
  *   lse        fp32 [B, Hq, T_max]     (out, may be NULL) entries u >= T not written
  *   ws         workspace of adapld_workspace_bytes(ADAPLD_OP_TREE_VERIFY_ATTN, B, L_stride, 0, 0, T_max, Hq, Hkv, D)
+ *              bytes (0 when the context is not split; ws may then be NULL)
  *
  * q, k and v must be finite (NaN or infinite inputs give undefined results);
  * scale must be finite and > 0 (the usual 1/sqrt(D)).
