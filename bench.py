@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "6c500a7bda61215f08b61d0e42f27efaf31860353b734f543c470d415a101b05",
+    "source_sha256": "a435cf5dad2390a9769d1ecf198bfb5bc6ce629d838eeae6370ba73fd6b7042c",
     "fetch_kib": 269412.9,
     "write_kib": 5392.1,
     "fetch_scale": 2.0,
