@@ -18,6 +18,12 @@ Four steps, per sequence, in the paper's order (Sec. 3.3 - 3.6, Algorithm 1):
 ``build_draft_tree``-- reuse construction (Sec. 3.5) organised as a draft tree
                        (Sec. 3.6): one branch per distinct successor token,
                        each a copied span; an ancestor-or-self mask.
+``build_draft_tree_paper`` -- the paper's own construction (Sec. 3.5,
+                       Algorithm 1): the main copy path of a lexical anchor,
+                       branch tokens from the target's top tokens after the
+                       anchor, and one successor token per branch retrieved
+                       by a lexical match of the branch token and a
+                       hidden-state rerank against the anchor.
 ``tree_verify_attn``-- tree-masked attention over the KV cache (Sec. 3.6,
                        tree attention after Medusa), softmax in float64.
 ``embedding_fallback`` -- the lexical/semantic backoff with the paper's own
@@ -52,6 +58,16 @@ reproduced workload differs from its text):
   cache and is not a query row);
 * verification keys for node u are all context keys 0..L-1 followed by the
   tree keys of u's ancestors-or-self in ascending node order;
+* in the paper's construction the anchor j* is the top of the ranked list;
+  the main path (lexical hit only) is M[j*+1 .. j*+l] with
+  l = min(S+1, L-1-j*); the branch tokens are the given top tokens after the
+  anchor in their order, without negatives, repeats and (lexical hit) the
+  main path's first token, at most W of them; a branch token b gets the
+  successor M[t*+1] where t* maximises cos(H[t-1], H[j*]) over the positions
+  t in [1, L-2] with M_t = b (lowest t among equal scores); a token with no
+  such position gets no successor (the token-embedding fallback is not
+  applied to successors); nodes: the main path as a chain, then each branch
+  token (depth 0) followed by its successor (depth 1);
 * the token-embedding fallback scores positions j in [0, L-2] (the paper's
   1 <= j < |M|, 1-based) by cos(e[M_j], e[M_{L-1}]) (a zero norm gives 0),
   keeps those >= tau in ascending order, and is used only when the lexical
@@ -236,6 +252,59 @@ def build_draft_tree(tokens: np.ndarray, kind: int, ranked, W: int, S: int):
             v = parent[v]
     return dict(token=token, parent=parent, depth=depth, src=src, T=T,
                 branches=branches, mask=mask)
+
+
+def build_draft_tree_paper(tokens: np.ndarray, bank: np.ndarray, kind: int, ranked, top_tokens, W: int, S: int):
+    """The paper's draft construction (Sec. 3.5, Eqs. (8)-(15); Algorithm 1).
+
+    tokens: (L,) ints; bank: (L, d) float64 hidden states; kind and ranked:
+    the retrieval outcome (ranked positions, best first); top_tokens: the
+    target's top tokens after the anchor j* = ranked[0], best first.
+    Returns the same dict as build_draft_tree; src is the memory position a
+    node copies, or -1 for a branch token (it comes from the model).
+    """
+    M = np.asarray(tokens)
+    L = int(M.shape[0])
+    token, parent, depth, src = [], [], [], []
+    if kind != KIND_NONE and len(ranked) > 0:
+        j = int(ranked[0])
+        main = list(range(j + 1, j + 1 + min(S + 1, L - 1 - j))) if kind == KIND_LEX else []
+        for dpt, p in enumerate(main):
+            token.append(int(M[p]))
+            parent.append(-1 if dpt == 0 else len(token) - 2)
+            depth.append(dpt)
+            src.append(p)
+        first = int(M[j + 1]) if main else None
+        branches = []
+        for b in top_tokens:
+            b = int(b)
+            if b < 0 or b in branches or b == first:
+                continue
+            branches.append(b)
+            if len(branches) == W:
+                break
+        for b in branches:
+            u = len(token)
+            token.append(b)
+            parent.append(-1)
+            depth.append(0)
+            src.append(-1)
+            C = [t for t in range(1, L - 1) if int(M[t]) == b]
+            if C:
+                s_b = cosine_rows(bank, [t - 1 for t in C], bank[j])
+                best = C[int(np.argmax(s_b))]   # first maximum: the lowest t
+                token.append(int(M[best + 1]))
+                parent.append(u)
+                depth.append(1)
+                src.append(best + 1)
+    T = len(token)
+    mask = np.zeros((T, T), dtype=bool)
+    for u in range(T):
+        v = u
+        while v != -1:
+            mask[u, v] = True
+            v = parent[v]
+    return dict(token=token, parent=parent, depth=depth, src=src, T=T, mask=mask)
 
 
 # --------------------------------------------------------------------------

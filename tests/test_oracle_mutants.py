@@ -14,7 +14,7 @@ from concurrent.futures import ThreadPoolExecutor
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle_lexical.py", "tests/test_oracle_semantic.py",
         "tests/test_oracle_tree.py", "tests/test_oracle_verify.py", "tests/test_oracle_accept.py",
-        "tests/test_oracle_embedding.py"]
+        "tests/test_oracle_embedding.py", "tests/test_oracle_tree_paper.py"]
 
 MUTANTS = [
     ("js = np.arange(n - 1, L - 1)", "js = np.arange(n - 1, L)"),              # anchor counts itself
@@ -45,6 +45,12 @@ MUTANTS = [
     ("    s = cosine_rows(emb, M[:L - 1], emb[int(M[L - 1])])", "    s = cosine_rows(emb, M[:L - 1], emb[int(M[L - 2])])"),
     ("        return KIND_LEX, [int(j) for j in cand]\n", "        pass\n"),   # semantic set despite a hit
     ("    C = [j for j in range(L - 1) if s[j] >= tau]", "    C = [j for j in range(L - 2) if s[j] >= tau]"),
+    ("                token.append(int(M[best + 1]))", "                token.append(int(M[best]))"),   # the branch token again
+    ("                s_b = cosine_rows(bank, [t - 1 for t in C], bank[j])", "                s_b = cosine_rows(bank, C, bank[j])"),
+    ("            if b < 0 or b in branches or b == first:", "            if b < 0 or b in branches:"),  # main token kept as a branch
+    ("            C = [t for t in range(1, L - 1) if int(M[t]) == b]", "            C = [t for t in range(0, L - 1) if int(M[t]) == b]"),
+    ("        main = list(range(j + 1, j + 1 + min(S + 1, L - 1 - j))) if kind == KIND_LEX else []",
+     "        main = list(range(j + 1, j + 1 + min(S, L - 1 - j))) if kind == KIND_LEX else []"),
 ]
 
 
