@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "a435cf5dad2390a9769d1ecf198bfb5bc6ce629d838eeae6370ba73fd6b7042c",
+    "source_sha256": "b54d32cbbe0918965972890133ac06891afcfc171ae8e51dd8dd115a91362ecb",
     "fetch_kib": 269412.9,
     "write_kib": 5392.1,
     "fetch_scale": 2.0,
@@ -295,6 +295,74 @@ def measure_embed(adapld, cfg, bufs, s, tokens, lens, x, steps, stream):
                     "not part of the step"}
 
 
+def measure_paper_tree(adapld, cfg, bufs, s, tokens, lens, x, steps, stream):
+    """The paper's draft construction (adapld_build_draft_tree_paper) next to
+    the ranked-list tree (adapld_build_draft_tree), each timed back to back
+    behind a spin kernel on the step's own retrieval results.  The target's
+    top-W table is synthetic, drawn on the GPU from a fixed seed: slot 0 is
+    the next context token (the target agreeing with the copy), the other
+    slots are tokens of random context positions."""
+    import torch
+    B, Ls, W = cfg.B, cfg.L, cfg.W
+    g = torch.Generator(device="cuda").manual_seed(4321)
+    idx = torch.randint(0, Ls, (B, Ls, W), generator=g, device="cuda")
+    idx[:, :, 0] = torch.clamp(torch.arange(Ls, device="cuda") + 1, max=Ls - 1)
+    top = torch.stack([tokens[b][idx[b]] for b in range(B)]).to(torch.int32).contiguous()
+    del idx
+    T_max = cfg.S + 1 + 2 * W
+    n = max(steps, 20)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(int(n * 100e3))
+        e0.record(stream)
+        for _ in range(n):
+            out = fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e3, out
+
+    def paper():
+        return adapld.build_draft_tree_paper(tokens, lens, s["bank"], bufs.topk_pos, bufs.topk_count, bufs.kind,
+                                             top, cfg.S, T_max)
+
+    def plain():
+        return adapld.build_draft_tree(tokens, lens, bufs.topk_pos, bufs.topk_count, bufs.kind, cfg.W, cfg.S,
+                                       cfg.T_max)
+
+    us_plain, _ = timed(plain)
+    us_paper, out = timed(paper)
+    T = out[4].cpu().numpy()
+    # algorithmic bytes: every sequence's context scanned once for the branch
+    # tokens, one bank row per occurrence plus the anchor's, the table row,
+    # the outputs (four int32 arrays and the mask rows)
+    tok = x["tokens"]
+    pos = bufs.topk_pos[:, 0].cpu().numpy()
+    cnt = bufs.topk_count.cpu().numpy()
+    kd = bufs.kind.cpu().numpy()
+    topn = top.cpu().numpy()
+    occ = 0
+    for b in range(B):
+        L = int(min(max(x["lens"][b], 0), Ls))
+        j = int(pos[b])
+        if cnt[b] < 1 or kd[b] == 0 or not 0 <= j <= L - 2:
+            continue
+        br = [t for t in dict.fromkeys(int(v) for v in topn[b, j])
+              if t >= 0 and not (kd[b] == 1 and t == tok[b, j + 1])]
+        occ += int(np.isin(tok[b, 1:max(L - 1, 1)], br).sum())
+    nw = (T_max + 63) // 64
+    byts = int(4 * int(np.clip(x["lens"], 0, Ls).sum()) + 2 * cfg.d * (occ + B) + 4 * W * B
+               + B * T_max * (16 + 8 * nw) + 4 * B)
+    del top
+    return {"call": "adapld_build_draft_tree_paper", "us": us_paper, "ranked_list_tree_us": us_plain,
+            "algorithmic_bytes": byts, "occurrence_rows": occ, "nodes_mean": float(T.mean()), "T_max": T_max,
+            "note": "the paper's construction (branch tokens from a synthetic top-W table, reranked successors) "
+                    "in place of the ranked-list tree; back-to-back calls; not part of the step"}
+
+
 def measure(adapld, cfg, name, make_inputs, args):
     import torch
     log(f"[bench] generating {name}")
@@ -386,10 +454,11 @@ def measure(adapld, cfg, name, make_inputs, args):
         graph_us = g0.elapsed_time(g1) / steps * 1e3
         del graphs
 
-    acc = emb = None
+    acc = emb = ptree = None
     if not args.no_extras:
         acc = measure_accept(adapld, cfg, bufs, sets[0], x["lens"], lens, node_count, steps, stream)
         emb = measure_embed(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
+        ptree = measure_paper_tree(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
 
     work = algorithmic_work(cfg, x["lens"], cand_count, node_count, node_depth)
     total_b, ver_b = work["total"], work["verify"]
@@ -428,6 +497,7 @@ def measure(adapld, cfg, name, make_inputs, args):
                      "algorithmic_bytes_per_launch": ver_b, "launch_us": ver_ms * 1e3},
         "accept": acc,
         "embedding_fallback": emb,
+        "paper_tree": ptree,
     }
     del sets, bufs
     torch.cuda.empty_cache()

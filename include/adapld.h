@@ -18,6 +18,11 @@
  *
  *   2'. adapld_semantic_topk_embed
  *
+ * call 3 has one with the paper's branch tokens from the target's top
+ * tokens and hidden-state-reranked successors (Sec. 3.5, Algorithm 1):
+ *
+ *   3'. adapld_build_draft_tree_paper
+ *
  * and, once the target's greedy tokens for the verified tree are known,
  *
  *   5. adapld_accept_greedy     greedy acceptance of the tree and compaction
@@ -79,6 +84,7 @@ extern "C" {
 #define ADAPLD_OP_BUILD_DRAFT_TREE 3
 #define ADAPLD_OP_TREE_VERIFY_ATTN 4
 #define ADAPLD_OP_SEMANTIC_TOPK_EMBED 5
+#define ADAPLD_OP_BUILD_DRAFT_TREE_PAPER 6
 
 /* Limits of this implementation (larger values return ADAPLD_ERR_UNSUPPORTED). */
 #define ADAPLD_MAX_NMAX 64
@@ -99,8 +105,9 @@ int adapld_last_hip_error(void);
 int adapld_version(void);
 
 /* Bytes of device workspace that `op` needs for these sizes (0 if none).
- * Arguments that an op does not use are ignored.  Returns 0 for invalid
- * sizes (the entry point itself reports the error). */
+ * Arguments that an op does not use are ignored; for
+ * ADAPLD_OP_BUILD_DRAFT_TREE_PAPER the `k` argument carries W.  Returns 0 for
+ * invalid sizes (the entry point itself reports the error). */
 size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_max,
                               int Hq, int Hkv, int D);
 
@@ -209,6 +216,51 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
                             int k, int W, int S, int T_max, int32_t* node_token,
                             int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
                             int32_t* node_count, uint64_t* tree_mask, hipStream_t stream);
+
+/*
+ * adapld_build_draft_tree_paper -- the paper's own draft construction
+ * (Sec. 3.5, Eqs. (8)-(15), Algorithm 1); an alternative to call 3 with the
+ * same outputs.
+ *
+ * The anchor is j* = topk_pos[b, 0] (no tree when topk_count[b] == 0, kind
+ * is NONE or j* is outside [0, L-2]).  Nodes, in this order:
+ *   - on a lexical hit (kind LEX) the main path: the chain M[j*+1 ..
+ *     j*+min(S+1, L-1-j*)], src = its memory positions;
+ *   - the branch tokens: the entries of top_tokens[b, j*, 0..W-1] that are
+ *     >= 0, not a repeat of an earlier entry and (on a lexical hit) not
+ *     M[j*+1], in table order; each is a depth-0 node with src = -1;
+ *   - right after each branch token c, its successor: among the occurrences
+ *     t in [1, L-2] with M[t] == c, the one whose preceding hidden state
+ *     bank[b, t-1] has the highest cosine with bank[b, j*] (ties: lowest t;
+ *     fp32 scores as in adapld_semantic_topk); the node is M[t+1] at depth 1
+ *     with src = t+1.  A branch token with no occurrence has no successor.
+ * Node arrays and tree_mask have the layouts of adapld_build_draft_tree;
+ * T <= (S+1) + 2W.  Entries at or beyond T are unspecified except the mask
+ * rows, which are 0.
+ *
+ *   tokens, lens      as in adapld_lexical_match
+ *   bank              bf16 [B, L_stride, d] hidden states, d a multiple of 8
+ *   topk_pos, topk_count, kind, k   the retrieval outcome (adapld_semantic_topk)
+ *   top_tokens int32 [B, L_stride, W]  the target's top-W tokens predicted
+ *                     after each position, best first; -1 marks an empty slot
+ *   W                 1..64 branch tokens;  S >= 0 main-path copy length
+ *   ws                workspace of adapld_workspace_bytes(
+ *                     ADAPLD_OP_BUILD_DRAFT_TREE_PAPER, B, L_stride, d, W, ...)
+ *                     (the k slot carries W), 16-byte aligned
+ *
+ * Errors: NULL_ARG; INVALID_ARG for bad sizes, T_max < (S+1) + 2W or
+ * misaligned bank/ws; UNSUPPORTED for k > ADAPLD_MAX_K, W > 64,
+ * d > ADAPLD_MAX_HIDDEN, T_max > ADAPLD_MAX_TREE_NODES,
+ * B*W > ADAPLD_MAX_SEMANTIC_BATCH or B*W*L_stride > INT32_MAX;
+ * WORKSPACE_TOO_SMALL.
+ */
+int adapld_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, const uint16_t* bank,
+                                  int d, const int32_t* topk_pos, const int32_t* topk_count,
+                                  const int32_t* kind, int k, const int32_t* top_tokens, int W,
+                                  int S, int B, int L_stride, int T_max, int32_t* node_token,
+                                  int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
+                                  int32_t* node_count, uint64_t* tree_mask, void* ws,
+                                  size_t ws_bytes, hipStream_t stream);
 
 /*
  * adapld_tree_verify_attn -- tree attention for verification (Sec. 3.6):

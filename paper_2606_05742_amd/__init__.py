@@ -6,6 +6,6 @@ it (argument marshalling only).  A missing library is an error, never a
 fallback.
 """
 from .binding import (  # noqa: F401
-    KIND_LEX, KIND_NONE, KIND_SEM, AdapldError, StepBuffers, accept_greedy, build_draft_tree, lexical_match,
-    load_library, semantic_topk, semantic_topk_embed, step, tree_verify_attn, verify_plan, workspace_bytes,
+    KIND_LEX, KIND_NONE, KIND_SEM, AdapldError, StepBuffers, accept_greedy, build_draft_tree, build_draft_tree_paper,
+    lexical_match, load_library, semantic_topk, semantic_topk_embed, step, tree_verify_attn, verify_plan, workspace_bytes,
 )

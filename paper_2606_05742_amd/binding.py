@@ -19,6 +19,7 @@ import torch
 KIND_NONE, KIND_LEX, KIND_SEM = 0, 1, 2
 OP_LEXICAL_MATCH, OP_SEMANTIC_TOPK, OP_BUILD_DRAFT_TREE, OP_TREE_VERIFY_ATTN = 1, 2, 3, 4
 OP_SEMANTIC_TOPK_EMBED = 5
+OP_BUILD_DRAFT_TREE_PAPER = 6
 HEAD_DIM = 128
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadapld.so")
@@ -56,6 +57,9 @@ SIGNATURES = {
         ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p]),
+    "adapld_build_draft_tree_paper": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int] + [ctypes.c_void_p] * 3
+                                      + [ctypes.c_int] + [ctypes.c_void_p] + [ctypes.c_int] * 5
+                                      + [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p]),
     "adapld_tree_verify_attn": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -224,6 +228,41 @@ def build_draft_tree(tokens, lens, topk_pos, topk_count, kind, W, S, T_max=None,
         _ptr(node_count, "node_count", i32, (B,)),
         _ptr(tree_mask, "tree_mask", (torch.int64, torch.uint64), (B, T_max, nw)), _stream(stream))
     _check(st, "adapld_build_draft_tree")
+    return node_token, node_parent, node_depth, node_src, node_count, tree_mask
+
+
+def build_draft_tree_paper(tokens, lens, bank, topk_pos, topk_count, kind, top_tokens, S, T_max=None, *,
+                           node_token=None, node_parent=None, node_depth=None, node_src=None, node_count=None,
+                           tree_mask=None, ws=None, stream=None):
+    """The paper's draft tree (main path, branch tokens from the target's top
+    tokens, reranked successors); returns (token, parent, depth, src, count,
+    mask).  top_tokens is int32 [B, L_stride, W]."""
+    lib = load_library()
+    B, L_stride, d = bank.shape
+    k = topk_pos.shape[1]
+    W = top_tokens.shape[2]
+    T_max = S + 1 + 2 * W if T_max is None else T_max
+    nw = (T_max + 63) // 64
+    dev = bank.device
+    mk = lambda t: torch.empty((B, T_max), dtype=torch.int32, device=dev) if t is None else t  # noqa: E731
+    node_token, node_parent, node_depth, node_src = mk(node_token), mk(node_parent), mk(node_depth), mk(node_src)
+    node_count = _i32(B, dev) if node_count is None else node_count
+    tree_mask = torch.empty((B, T_max, nw), dtype=torch.int64, device=dev) if tree_mask is None else tree_mask
+    need = workspace_bytes(OP_BUILD_DRAFT_TREE_PAPER, B, L_stride, d, W)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    i32 = (torch.int32,)
+    st = lib.adapld_build_draft_tree_paper(
+        _ptr(tokens, "tokens", i32, (B, L_stride)), _ptr(lens, "lens", i32, (B,)), _ptr(bank, "bank", _BF16_DTYPES),
+        d, _ptr(topk_pos, "topk_pos", i32, (B, k)), _ptr(topk_count, "topk_count", i32, (B,)),
+        _ptr(kind, "kind", i32, (B,)), k, _ptr(top_tokens, "top_tokens", i32, (B, L_stride, W)), W, S, B,
+        L_stride, T_max,
+        _ptr(node_token, "node_token", i32, (B, T_max)), _ptr(node_parent, "node_parent", i32, (B, T_max)),
+        _ptr(node_depth, "node_depth", i32, (B, T_max)), _ptr(node_src, "node_src", i32, (B, T_max)),
+        _ptr(node_count, "node_count", i32, (B,)),
+        _ptr(tree_mask, "tree_mask", (torch.int64, torch.uint64), (B, T_max, nw)),
+        _ptr(ws, "ws", (torch.uint8,)), ws.numel(), _stream(stream))
+    _check(st, "adapld_build_draft_tree_paper")
     return node_token, node_parent, node_depth, node_src, node_count, tree_mask
 
 

@@ -48,7 +48,6 @@ int adapld_version(void) { return kVersion; }
 
 size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_max, int Hq, int Hkv,
                               int D) {
-  (void)d;
   (void)D;
   if (B <= 0 || L_stride <= 0) return 0;
   switch (op) {
@@ -58,6 +57,9 @@ size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_m
     case ADAPLD_OP_SEMANTIC_TOPK_EMBED:
       if (k < 1 || k > ADAPLD_MAX_K) return 0;
       return embed_head_ws(B, L_stride) + semantic_ws(B, L_stride, k);
+    case ADAPLD_OP_BUILD_DRAFT_TREE_PAPER:   // k carries W
+      if (k < 1 || k > 64 || d < 8 || d % 8 || (int64_t)B * k > ADAPLD_MAX_SEMANTIC_BATCH) return 0;
+      return adapld::paper_tree_ws_bytes(B, L_stride, k, d);
     case ADAPLD_OP_TREE_VERIFY_ATTN: {
       if (T_max < 1 || T_max > ADAPLD_MAX_TREE_NODES || Hq < 1 || Hkv < 1 || Hq % Hkv) return 0;
       const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
@@ -162,6 +164,31 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
                                                     L_stride, k, W, S, T_max, node_token,
                                                     node_parent, node_depth, node_src, node_count,
                                                     tree_mask, stream));
+}
+
+int adapld_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, const uint16_t* bank,
+                                  int d, const int32_t* topk_pos, const int32_t* topk_count,
+                                  const int32_t* kind, int k, const int32_t* top_tokens, int W,
+                                  int S, int B, int L_stride, int T_max, int32_t* node_token,
+                                  int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
+                                  int32_t* node_count, uint64_t* tree_mask, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!tokens || !lens || !bank || !topk_pos || !topk_count || !kind || !top_tokens ||
+      !node_token || !node_parent || !node_depth || !node_src || !node_count || !tree_mask || !ws)
+    return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || d < 8 || d % 8 != 0 || k < 1 || W < 1 || S < 0 || T_max < 1)
+    return ADAPLD_ERR_INVALID_ARG;
+  if (k > ADAPLD_MAX_K || W > 64 || d > ADAPLD_MAX_HIDDEN || T_max > ADAPLD_MAX_TREE_NODES ||
+      (int64_t)B * W > ADAPLD_MAX_SEMANTIC_BATCH || (int64_t)B * W * L_stride > INT32_MAX)
+    return ADAPLD_ERR_UNSUPPORTED;
+  if ((int64_t)S + 1 + 2LL * W > T_max) return ADAPLD_ERR_INVALID_ARG;
+  if (misaligned16(bank) || misaligned16(ws)) return ADAPLD_ERR_INVALID_ARG;
+  if (ws_bytes < adapld::paper_tree_ws_bytes(B, L_stride, W, d)) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  return hip_status(adapld::launch_build_draft_tree_paper(
+      tokens, lens, bank, d, topk_pos, topk_count, kind, k, top_tokens, W, S, B, L_stride, T_max,
+      node_token, node_parent, node_depth, node_src, node_count, tree_mask, ws, stream));
 }
 
 int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx,

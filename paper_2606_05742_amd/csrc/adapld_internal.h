@@ -56,7 +56,7 @@ hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, con
                                 int L_stride, int d, int k, float tau, int32_t* topk_pos,
                                 float* topk_score, int32_t* topk_count, int32_t* kind,
                                 uint64_t* ws_keys, const int32_t* cand_kind, int rerank_only,
-                                hipStream_t stream);
+                                hipStream_t stream, int seq_div = 1);
 
 hipError_t launch_build_draft_tree(const int32_t* tokens, const int32_t* lens,
                                    const int32_t* topk_pos, const int32_t* topk_count,
@@ -73,6 +73,18 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
                                    void* ws, const VerifyPlan& plan, hipStream_t stream);
 
 size_t embed_ws_bytes(int B, int L_stride);
+
+// The paper's draft construction: branch tokens from the target's top tokens
+// after the anchor, each followed by its hidden-state-reranked successor.
+// Workspace: branch tokens, per-branch candidate lists and queries, and the
+// rerank's lists.
+size_t paper_tree_ws_bytes(int B, int L_stride, int W, int d);
+hipError_t launch_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, const uint16_t* bank, int d,
+                                         const int32_t* topk_pos, const int32_t* topk_count, const int32_t* kind,
+                                         int k, const int32_t* top_tokens, int W, int S, int B, int L_stride,
+                                         int T_max, int32_t* node_token, int32_t* node_parent, int32_t* node_depth,
+                                         int32_t* node_src, int32_t* node_count, uint64_t* tree_mask, void* ws,
+                                         hipStream_t stream);
 
 // Writes the lexical/embedding candidate set, its size and its kind into ws
 // and returns pointers to them.

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     for n in names:
         assert hasattr(lib, n), n
         assert n in binding.SIGNATURES, n
@@ -96,6 +96,34 @@ def test_embed_validation(lib):
     need = lib.adapld_workspace_bytes(5, 2, 64, 128, 8, 0, 0, 0, 0)
     assert need >= lib.adapld_workspace_bytes(2, 2, 64, 128, 8, 0, 0, 0, 0) + 2 * 64 * 5
     assert f(*args(ws_bytes=need - 1)) == WS_SMALL
+
+
+def test_paper_tree_validation(lib):
+    f = lib.adapld_build_draft_tree_paper
+    args = lambda **kw: [kw.get(n, v) for n, v in (  # noqa: E731
+        ("tokens", P), ("lens", P), ("bank", P), ("d", 128), ("pos", P), ("count", P), ("kind", P), ("k", 8),
+        ("top", P), ("W", 4), ("S", 12), ("B", 2), ("L_stride", 64), ("T_max", 21),
+        ("nt", P), ("np", P), ("nd", P), ("ns", P), ("nc", P), ("mask", P), ("ws", P), ("ws_bytes", 1 << 30),
+        ("stream", N))]
+    assert f(*args(B=0)) == OK
+    assert f(*args(B=-1)) == INVALID
+    assert f(*args(bank=N)) == NULL
+    assert f(*args(top=N)) == NULL
+    assert f(*args(ws=N)) == NULL
+    assert f(*args(d=12)) == INVALID
+    assert f(*args(W=0)) == INVALID
+    assert f(*args(S=-1)) == INVALID
+    assert f(*args(T_max=20)) == INVALID                  # below (S+1) + 2W
+    assert f(*args(W=65, T_max=256)) == UNSUPPORTED
+    assert f(*args(k=65)) == UNSUPPORTED
+    assert f(*args(T_max=257)) == UNSUPPORTED
+    assert f(*args(B=513)) == UNSUPPORTED                 # B*W lists > 2048
+    assert f(*args(bank=ctypes.c_void_p(0x10008))) == INVALID
+    assert f(*args(ws=ctypes.c_void_p(0x10008))) == INVALID
+    need = lib.adapld_workspace_bytes(6, 2, 64, 128, 4, 0, 0, 0, 0)
+    assert need >= 2 * 4 * 64 * 4 + 2 * 4 * 128 * 2     # candidate lists + queries
+    assert f(*args(ws_bytes=need - 1)) == WS_SMALL
+    assert lib.adapld_workspace_bytes(6, 2, 64, 12, 4, 0, 0, 0, 0) == 0
 
 
 def test_accept_validation(lib):
