@@ -9,10 +9,11 @@
 // main path's first token on a lexical hit).  Then every thread scans part
 // of the context once for all branch tokens together: each occurrence t in
 // [1, L-2] of branch token i appends row t-1 to candidate list (b, i).  The
-// list's query is the anchor's hidden state H[j*], copied next to it.
+// W lists of a sequence share one query, the anchor's hidden state H[j*],
+// copied once per sequence.
 //
 // rerank: the hidden-state scan and merge with k = 1 over the B*W lists (a
-// list reads the bank rows of its sequence), so the argmax of
+// list reads the bank rows and the query of its sequence), so the argmax of
 // cos(H[t-1], H[j*]) costs one pass over the candidate rows of all branches
 // of all sequences, spread over the whole GPU.
 //
@@ -42,7 +43,7 @@ struct PaperTreeArgs {
   int32_t* vcand;    // [B*W][L_stride] candidate rows t-1
   int32_t* vcount;   // [B*W]
   int32_t* vlens;    // [B*W]  the sequence's L
-  uint16_t* vquery;  // [B*W][d] H[j*]
+  uint16_t* vquery;  // [B][d]   H[j*], the query of the sequence's W lists
   int32_t* vpos;     // [B*W]  the winning row (k = 1)
   float* vscore;
   int32_t* vcnt;     // [B*W]  1 if the branch has a successor
@@ -60,10 +61,17 @@ struct PaperTreeArgs {
 // anchor without a following token).
 __device__ __forceinline__ int anchor_of(const PaperTreeArgs& a, int b, int L, int& kd) {
   kd = a.kind[b];
-  const int cnt = min(max(a.topk_count[b], 0), a.k);
-  const int j = cnt > 0 && kd != ADAPLD_KIND_NONE ? a.topk_pos[(size_t)b * a.k] : -1;
+  const int cnt = a.topk_count[b];
+  const int j0 = a.topk_pos[(size_t)b * a.k];   // in bounds for every b: read without waiting for cnt
+  const int j = cnt > 0 && kd != ADAPLD_KIND_NONE ? j0 : -1;
   return j >= 0 && j <= L - 2 ? j : -1;
 }
+
+// Tokens a setup thread holds per pass: kSetupVec 16-byte loads, coalesced
+// across the workgroup (thread x loads int4 number i*kSetupThreads + x).
+constexpr int kSetupVec = 8;
+constexpr int kSetupPass = kSetupThreads * kSetupVec * 4;
+constexpr int kQueryVec = (ADAPLD_MAX_HIDDEN / 8 + kSetupThreads - 1) / kSetupThreads;
 
 __global__ __launch_bounds__(kSetupThreads) void paper_tree_setup_kernel(const PaperTreeArgs a) {
   __shared__ int s_tok[kWave];
@@ -74,8 +82,56 @@ __global__ __launch_bounds__(kSetupThreads) void paper_tree_setup_kernel(const P
   const int lane = lane_id();
   const int L = min(max(a.lens[b], 0), a.L_stride);
   const int32_t* __restrict__ M = a.tokens + (size_t)b * a.L_stride;
+  // The first pass's tokens are requested before the anchor and L are known:
+  // every load stays inside the row (L_stride tokens) and positions at or
+  // beyond L are masked afterwards.  A whole pass over a 16-byte-aligned row
+  // loads int4s; any other pass loads single tokens at clamped positions.
+  // Both forms are branch-free so that all loads of a pass are in flight
+  // together.
+  const bool vec = (reinterpret_cast<uintptr_t>(M) & 15) == 0;
+  int4 cur[kSetupVec];
+  auto load_pass = [&](int base) {
+    if (vec && base + kSetupPass <= a.L_stride) {
+#pragma unroll
+      for (int i = 0; i < kSetupVec; ++i)
+        cur[i] = *reinterpret_cast<const int4*>(M + base + 4 * (i * kSetupThreads + tid));
+    } else {
+      const int last = a.L_stride - 1;
+#pragma unroll
+      for (int i = 0; i < kSetupVec; ++i) {
+        const int t0 = base + 4 * (i * kSetupThreads + tid);
+        cur[i].x = M[min(t0, last)];
+        cur[i].y = M[min(t0 + 1, last)];
+        cur[i].z = M[min(t0 + 2, last)];
+        cur[i].w = M[min(t0 + 3, last)];
+      }
+    }
+  };
+  load_pass(0);
   int kd;
   const int j = anchor_of(a, b, L, kd);
+  // The anchor's hidden state, the query of all its branch lists, copied
+  // while the branch tokens are chosen (d/8 <= kSetupThreads * kQueryVec
+  // 16-byte chunks; row max(j, 0) and clamped chunks keep the loads in
+  // bounds and branch-free).
+  {
+    const int chunks = a.d / 8;
+    const uint4* __restrict__ src =
+        reinterpret_cast<const uint4*>(a.bank + ((size_t)b * a.L_stride + max(j, 0)) * a.d);
+    uint4* __restrict__ dst = reinterpret_cast<uint4*>(a.vquery + (size_t)b * a.d);
+    // (four named registers: an array here would be placed in LDS)
+    static_assert(kQueryVec == 4, "query chunks per thread");
+    const uint4 q0 = src[min(tid, chunks - 1)];
+    const uint4 q1 = src[min(tid + kSetupThreads, chunks - 1)];
+    const uint4 q2 = src[min(tid + 2 * kSetupThreads, chunks - 1)];
+    const uint4 q3 = src[min(tid + 3 * kSetupThreads, chunks - 1)];
+    if (j >= 0) {
+      if (tid < chunks) dst[tid] = q0;
+      if (tid + kSetupThreads < chunks) dst[tid + kSetupThreads] = q1;
+      if (tid + 2 * kSetupThreads < chunks) dst[tid + 2 * kSetupThreads] = q2;
+      if (tid + 3 * kSetupThreads < chunks) dst[tid + 3 * kSetupThreads] = q3;
+    }
+  }
   if (tid < kWave) {
     // Branch tokens: the valid, distinct top tokens after the anchor, in order.
     int tok = -1;
@@ -101,13 +157,47 @@ __global__ __launch_bounds__(kSetupThreads) void paper_tree_setup_kernel(const P
   __syncthreads();
   const int nb = s_nb;
   // One pass over the context for all branch tokens: occurrence t (with a
-  // preceding hidden state and a following token) of branch i adds row t-1.
-  for (int t = 1 + tid; t <= L - 2 && nb > 0; t += kSetupThreads) {
-    const int m = M[t];
-    for (int i = 0; i < nb; ++i) {
-      if (m == s_tok[i]) {
-        const int slot = atomicAdd(&s_cnt[i], 1);
-        a.vcand[((size_t)b * a.W + i) * a.L_stride + slot] = t - 1;
+  // preceding hidden state and a following token, t in [1, L-2]) of branch i
+  // adds row t-1 to list i.  Per branch a thread compares its tokens in
+  // registers into a 32-bit mask, takes that many slots and writes the rows.
+  // List order is arbitrary: the rerank breaks ties by position.
+  for (int base = 0; nb > 0 && base < L; base += kSetupPass) {
+    if (base > 0) load_pass(base);
+    uint32_t valid = 0;   // bit 4i+e: token e of load i is an occurrence position
+#pragma unroll
+    for (int i = 0; i < kSetupVec; ++i) {
+      const int t0 = base + 4 * (i * kSetupThreads + tid);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) valid |= (t0 + e >= 1 && t0 + e <= L - 2 ? 1u : 0u) << (4 * i + e);
+    }
+    for (int br = 0; br < nb; ++br) {
+      const int c = s_tok[br];
+      uint32_t hit = 0;
+#pragma unroll
+      for (int i = 0; i < kSetupVec; ++i) {
+        hit |= (cur[i].x == c ? 1u : 0u) << (4 * i);
+        hit |= (cur[i].y == c ? 1u : 0u) << (4 * i + 1);
+        hit |= (cur[i].z == c ? 1u : 0u) << (4 * i + 2);
+        hit |= (cur[i].w == c ? 1u : 0u) << (4 * i + 3);
+      }
+      hit &= valid;
+      // Slots: a prefix sum of the hit counts over the wave and one LDS
+      // atomic per wave (a per-lane atomic with per-lane operands costs a
+      // loop over the active lanes).
+      const int n = __popc(hit);
+      const int incl = wave_incl_scan_i32(n);
+      const int total = __builtin_amdgcn_readlane(incl, kWave - 1);
+      if (total > 0) {
+        int first = 0;
+        if (lane == kWave - 1) first = atomicAdd(&s_cnt[br], total);
+        int slot = __builtin_amdgcn_readlane(first, kWave - 1) + incl - n;
+        int32_t* __restrict__ dst = a.vcand + ((size_t)b * a.W + br) * a.L_stride;
+        while (hit) {
+          const int bit = __builtin_ctz(hit);
+          hit &= hit - 1;
+          const int t = base + 4 * ((bit >> 2) * kSetupThreads + tid) + (bit & 3);
+          dst[slot++] = t - 1;
+        }
       }
     }
   }
@@ -116,16 +206,6 @@ __global__ __launch_bounds__(kSetupThreads) void paper_tree_setup_kernel(const P
     const size_t v = (size_t)b * a.W + tid;
     a.vcount[v] = tid < nb ? s_cnt[tid] : 0;
     a.vlens[v] = L;
-  }
-  // The lists' query: the anchor's hidden state, 16 bytes at a time.
-  if (j >= 0) {
-    const int chunks = a.d / 8;
-    const uint4* __restrict__ src = reinterpret_cast<const uint4*>(a.bank + ((size_t)b * a.L_stride + j) * a.d);
-    for (int idx = tid; idx < nb * chunks; idx += kSetupThreads) {
-      const int i = idx / chunks;
-      const int c = idx - i * chunks;
-      reinterpret_cast<uint4*>(a.vquery + ((size_t)b * a.W + i) * a.d)[c] = src[c];
-    }
   }
 }
 
@@ -210,7 +290,7 @@ size_t paper_tree_ws_bytes(int B, int L_stride, int W, int d) {
   n += V * L_stride * 4;                 // vcand
   n += V * 4 * 2;                        // vcount, vlens
   n = (n + 15) / 16 * 16;
-  n += V * d * 2;                        // vquery
+  n += (size_t)B * d * 2;                // vquery
   n += V * 4 * 4;                        // vpos, vscore, vcnt, vkind
   n = (n + 15) / 16 * 16;
   n += V * scan_lists(L_stride) * 8;     // the rerank's lists (k = 1)
@@ -236,7 +316,7 @@ hipError_t launch_build_draft_tree_paper(const int32_t* tokens, const int32_t* l
   a.vcount = reinterpret_cast<int32_t*>(p + off); off += V * 4;
   a.vlens = reinterpret_cast<int32_t*>(p + off); off += V * 4;
   off = (off + 15) / 16 * 16;
-  a.vquery = reinterpret_cast<uint16_t*>(p + off); off += V * d * 2;
+  a.vquery = reinterpret_cast<uint16_t*>(p + off); off += (size_t)B * d * 2;
   a.vpos = reinterpret_cast<int32_t*>(p + off); off += V * 4;
   a.vscore = reinterpret_cast<float*>(p + off); off += V * 4;
   a.vcnt = reinterpret_cast<int32_t*>(p + off); off += V * 4;

@@ -52,7 +52,7 @@ struct ScanArgs {
   uint64_t* ws_keys;              // [B][lists][k]
   const int32_t* cand_kind;       // kind of a non-empty candidate set (NULL: LEX)
   int rerank_only;                // 1: an empty candidate set scores nothing (kind NONE)
-  int seq_div;                    // candidate list s reads the bank rows of sequence s / seq_div
+  int seq_div;                    // list s reads the bank rows and query of sequence s / seq_div
 };
 
 __device__ __forceinline__ void seq_rows(const ScanArgs& a, int b, int& L, int& cc, int& nrows) {
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const Sc
     mine = 0;
   };
   auto query_of = [&](int b) {
-    return a.query ? a.query + (size_t)b * d
+    return a.query ? a.query + (size_t)(b / a.seq_div) * d
                    : a.bank + ((size_t)(b / a.seq_div) * a.L_stride + max(s_len[b] - 1, 0)) * d;
   };
   auto begin_segment = [&](int g) {
