@@ -13,6 +13,9 @@
  *                               (Sec. 3.5, Sec. 3.6)
  *   4. adapld_tree_verify_attn  tree-masked verify attention (Sec. 3.6)
  *
+ * adapld_step enqueues calls 1-4 in that order with one host call (Algorithm
+ * 1's draft-and-verify iteration), after validating all four.
+ *
  * Call 2 has a drop-in alternative with the paper's own semantic signal,
  * token-embedding similarity (Sec. 3.3, Eq. (4)):
  *
@@ -85,6 +88,7 @@ extern "C" {
 #define ADAPLD_OP_TREE_VERIFY_ATTN 4
 #define ADAPLD_OP_SEMANTIC_TOPK_EMBED 5
 #define ADAPLD_OP_BUILD_DRAFT_TREE_PAPER 6
+#define ADAPLD_OP_STEP 7
 
 /* Limits of this implementation (larger values return ADAPLD_ERR_UNSUPPORTED). */
 #define ADAPLD_MAX_NMAX 64
@@ -216,6 +220,32 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
                             int k, int W, int S, int T_max, int32_t* node_token,
                             int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
                             int32_t* node_count, uint64_t* tree_mask, hipStream_t stream);
+
+/*
+ * adapld_step -- one draft-and-verify iteration (Algorithm 1, between two
+ * target forward passes): adapld_lexical_match, adapld_semantic_topk,
+ * adapld_build_draft_tree and adapld_tree_verify_attn enqueued on `stream`
+ * in that order, with no host synchronisation.  Every argument has the
+ * meaning, layout and limits it has in those four calls (n_max for the
+ * lexical match; d, k, tau and query for the rerank; W, S and T_max for the
+ * tree; Hq, Hkv, D and scale for the verify; T_max is also the verify's).
+ * All four argument sets are validated before anything is enqueued; the
+ * status is that of the first failing check, or of the first failing launch.
+ *
+ *   ws   workspace of adapld_workspace_bytes(ADAPLD_OP_STEP, B, L_stride, d, k,
+ *        T_max, Hq, Hkv, D), 16-byte aligned: the rerank's lists, then the
+ *        verify's partials
+ *
+ * Outputs are those of the four calls.
+ */
+int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank, const uint16_t* query,
+                const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx, const uint16_t* k_tree,
+                const uint16_t* v_tree, int B, int L_stride, int d, int n_max, int k, int W, int S,
+                int T_max, int Hq, int Hkv, int D, float tau, float scale, int32_t* cand_pos,
+                int32_t* cand_count, int32_t* match_n, int32_t* topk_pos, float* topk_score,
+                int32_t* topk_count, int32_t* kind, int32_t* node_token, int32_t* node_parent,
+                int32_t* node_depth, int32_t* node_src, int32_t* node_count, uint64_t* tree_mask,
+                uint16_t* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * adapld_build_draft_tree_paper -- the paper's own draft construction

@@ -20,6 +20,7 @@ KIND_NONE, KIND_LEX, KIND_SEM = 0, 1, 2
 OP_LEXICAL_MATCH, OP_SEMANTIC_TOPK, OP_BUILD_DRAFT_TREE, OP_TREE_VERIFY_ATTN = 1, 2, 3, 4
 OP_SEMANTIC_TOPK_EMBED = 5
 OP_BUILD_DRAFT_TREE_PAPER = 6
+OP_STEP = 7
 HEAD_DIM = 128
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadapld.so")
@@ -57,6 +58,8 @@ SIGNATURES = {
         ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p]),
+    "adapld_step": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 11 + [ctypes.c_float] * 2
+                    + [ctypes.c_void_p] * 16 + [ctypes.c_size_t, ctypes.c_void_p]),
     "adapld_build_draft_tree_paper": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int] + [ctypes.c_void_p] * 3
                                       + [ctypes.c_int] + [ctypes.c_void_p] + [ctypes.c_int] * 5
                                       + [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p]),
@@ -353,15 +356,16 @@ class StepBuffers:
     lse: torch.Tensor
     ws_sem: torch.Tensor
     ws_ver: torch.Tensor
+    ws_step: torch.Tensor    # ws_sem and ws_ver are views of it (the layout adapld_step expects)
 
     @staticmethod
     def allocate(B, L_stride, d, k, T_max, Hq, Hkv, D=HEAD_DIM, device="cuda"):
         i32 = lambda *s: torch.empty(s, dtype=torch.int32, device=device)  # noqa: E731
         nw = (T_max + 63) // 64
-        ws_sem = torch.empty(max(workspace_bytes(OP_SEMANTIC_TOPK, B, L_stride, d, k), 16),
-                             dtype=torch.uint8, device=device)
-        ws_ver = torch.empty(max(workspace_bytes(OP_TREE_VERIFY_ATTN, B, L_stride, 0, 0, T_max, Hq, Hkv, D), 16),
-                             dtype=torch.uint8, device=device)
+        sem = (workspace_bytes(OP_SEMANTIC_TOPK, B, L_stride, d, k) + 255) // 256 * 256
+        ver = workspace_bytes(OP_TREE_VERIFY_ATTN, B, L_stride, 0, 0, T_max, Hq, Hkv, D)
+        ws_step = torch.empty(sem + max(ver, 16), dtype=torch.uint8, device=device)
+        ws_sem, ws_ver = ws_step[:sem], ws_step[sem:]
         return StepBuffers(
             cand_pos=i32(B, L_stride), cand_count=i32(B), match_n=i32(B),
             topk_pos=i32(B, k), topk_score=torch.empty((B, k), dtype=torch.float32, device=device),
@@ -371,16 +375,73 @@ class StepBuffers:
             tree_mask=torch.empty((B, T_max, nw), dtype=torch.int64, device=device),
             out=torch.empty((B, T_max, Hq, D), dtype=torch.bfloat16, device=device),
             lse=torch.empty((B, Hq, T_max), dtype=torch.float32, device=device),
-            ws_sem=ws_sem, ws_ver=ws_ver)
+            ws_sem=ws_sem, ws_ver=ws_ver, ws_step=ws_step)
+
+
+class StepCall:
+    """One draft-and-verify step as a single native call (adapld_step, which
+    enqueues the four kernels on one stream).  The tensors are checked and
+    their pointers marshalled once, here; every call() then costs one C call.
+    The stream is the one given, else the current stream at construction."""
+
+    def __init__(self, tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None,
+                 query=None, scale=None, buffers: StepBuffers | None = None, stream=None):
+        B, L_stride = tokens.shape
+        _, _, d = bank.shape
+        _, T_max, Hq, D = q.shape
+        Hkv = k_ctx.shape[1]
+        if buffers is None:
+            buffers = StepBuffers.allocate(B, L_stride, d, k, T_max, Hq, Hkv, D, device=tokens.device)
+        bf = self.buffers = buffers
+        need = workspace_bytes(OP_STEP, B, L_stride, d, k, T_max, Hq, Hkv, D)
+        if bf.ws_step.numel() < need:
+            raise AdapldError(-4, f"buffers.ws_step holds {bf.ws_step.numel()} bytes, {need} needed")
+        scale = 1.0 / math.sqrt(D) if scale is None else scale
+        tau = float("nan") if tau is None else float(tau)
+        i32, bf16 = (torch.int32,), _BF16_DTYPES
+        nw = (T_max + 63) // 64
+        self._fn = load_library().adapld_step
+        self._args = (
+            _ptr(tokens, "tokens", i32, (B, L_stride)), _ptr(lens, "lens", i32, (B,)),
+            _ptr(bank, "bank", bf16), _ptr(query, "query", bf16, (B, d), nullable=True),
+            _ptr(q, "q", bf16), _ptr(k_ctx, "k_ctx", bf16, (B, Hkv, L_stride, D)),
+            _ptr(v_ctx, "v_ctx", bf16, (B, Hkv, L_stride, D)), _ptr(k_tree, "k_tree", bf16, (B, T_max, Hkv, D)),
+            _ptr(v_tree, "v_tree", bf16, (B, T_max, Hkv, D)),
+            B, L_stride, d, n_max, k, W, S, T_max, Hq, Hkv, D, tau, scale,
+            _ptr(bf.cand_pos, "cand_pos", i32, (B, L_stride)), _ptr(bf.cand_count, "cand_count", i32, (B,)),
+            _ptr(bf.match_n, "match_n", i32, (B,)), _ptr(bf.topk_pos, "topk_pos", i32, (B, k)),
+            _ptr(bf.topk_score, "topk_score", (torch.float32,), (B, k)),
+            _ptr(bf.topk_count, "topk_count", i32, (B,)), _ptr(bf.kind, "kind", i32, (B,)),
+            _ptr(bf.node_token, "node_token", i32, (B, T_max)), _ptr(bf.node_parent, "node_parent", i32, (B, T_max)),
+            _ptr(bf.node_depth, "node_depth", i32, (B, T_max)), _ptr(bf.node_src, "node_src", i32, (B, T_max)),
+            _ptr(bf.node_count, "node_count", i32, (B,)),
+            _ptr(bf.tree_mask, "tree_mask", (torch.int64, torch.uint64), (B, T_max, nw)),
+            _ptr(bf.out, "out", bf16, (B, T_max, Hq, D)), _ptr(bf.lse, "lse", (torch.float32,), (B, Hq, T_max)),
+            _ptr(bf.ws_step, "ws_step", (torch.uint8,)), bf.ws_step.numel(), _stream(stream))
+        # keep every tensor alive as long as the call can be made
+        self._keep = (tokens, lens, bank, query, q, k_ctx, v_ctx, k_tree, v_tree)
+
+    def __call__(self) -> StepBuffers:
+        _check(self._fn(*self._args), "adapld_step")
+        return self.buffers
 
 
 def step(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None, query=None,
          scale=None, buffers: StepBuffers | None = None, stream=None):
-    """One draft-and-verify step: the four entry points back to back on one stream.
+    """One draft-and-verify step: adapld_step, i.e. the four entry points
+    back to back on one stream from one native call.
 
     No host synchronisation happens inside; the lexical-hit / fallback decision
     is taken on the device.  Returns the StepBuffers holding every output.
     """
+    return StepCall(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, n_max=n_max, k=k, W=W, S=S, tau=tau,
+                    query=query, scale=scale, buffers=buffers, stream=stream)()
+
+
+def step_calls(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None, query=None,
+               scale=None, buffers: StepBuffers | None = None, stream=None):
+    """The same step as four separate entry-point calls (the route a caller
+    takes to put its own work or events between them)."""
     B, L_stride = tokens.shape
     T_max = q.shape[1]
     if buffers is None:

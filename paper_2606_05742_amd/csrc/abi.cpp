@@ -23,8 +23,82 @@ size_t semantic_ws(int B, int L_stride, int k) {
   return (size_t)B * adapld::scan_lists(L_stride) * k * sizeof(uint64_t);
 }
 
+// adapld_step: the scan's lists first (rounded to 256 bytes), then the verify
+// workspace.
+size_t step_sem_part(int B, int L_stride, int k) { return (semantic_ws(B, L_stride, k) + 255) / 256 * 256; }
+
 // The embedding fallback's own part (16-byte aligned), then the scan's lists.
 size_t embed_head_ws(int B, int L_stride) { return (adapld::embed_ws_bytes(B, L_stride) + 15) / 16 * 16; }
+
+// Host-side validation of each entry point (shared with adapld_step); B == 0
+// is a valid, empty call.
+int check_lexical(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                  int32_t* cand_pos, int32_t* cand_count, int32_t* match_n) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!tokens || !lens || !cand_pos || !cand_count || !match_n) return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1) return ADAPLD_ERR_INVALID_ARG;
+  if (n_max < 1 || n_max > ADAPLD_MAX_NMAX) return ADAPLD_ERR_UNSUPPORTED;
+  return ADAPLD_OK;
+}
+
+int check_semantic(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
+                   const int32_t* cand_pos, const int32_t* cand_count, int B, int L_stride,
+                   int d, int k, float tau, int32_t* topk_pos, float* topk_score,
+                   int32_t* topk_count, int32_t* kind, void* ws, size_t ws_bytes) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!bank || !lens || !cand_pos || !cand_count || !topk_pos || !topk_score || !topk_count ||
+      !kind || !ws)
+    return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || d < 8 || d % 8 != 0 || k < 1) return ADAPLD_ERR_INVALID_ARG;
+  if (d > ADAPLD_MAX_HIDDEN || k > ADAPLD_MAX_K || B > ADAPLD_MAX_SEMANTIC_BATCH ||
+      (int64_t)B * L_stride > INT32_MAX)
+    return ADAPLD_ERR_UNSUPPORTED;
+  if (misaligned16(bank) || (query && misaligned16(query))) return ADAPLD_ERR_INVALID_ARG;
+  if (ws_bytes < semantic_ws(B, L_stride, k)) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  return ADAPLD_OK;
+}
+
+int check_tree(const int32_t* tokens, const int32_t* lens, const int32_t* topk_pos,
+               const int32_t* topk_count, const int32_t* kind, int B, int L_stride,
+               int k, int W, int S, int T_max, int32_t* node_token,
+               int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
+               int32_t* node_count, uint64_t* tree_mask) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!tokens || !lens || !topk_pos || !topk_count || !kind || !node_token || !node_parent ||
+      !node_depth || !node_src || !node_count || !tree_mask)
+    return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || k < 1 || W < 1 || S < 0 || T_max < 1) return ADAPLD_ERR_INVALID_ARG;
+  if (k > ADAPLD_MAX_K || T_max > ADAPLD_MAX_TREE_NODES) return ADAPLD_ERR_UNSUPPORTED;
+  if ((long long)W * (S + 1LL) > T_max) return ADAPLD_ERR_INVALID_ARG;
+  return ADAPLD_OK;
+}
+
+int check_verify(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx,
+                 const uint16_t* k_tree, const uint16_t* v_tree, const int32_t* lens,
+                 const int32_t* node_count, const uint64_t* tree_mask, int B,
+                 int L_stride, int T_max, int Hq, int Hkv, int D, float scale,
+                 uint16_t* out, float* lse, void* ws, size_t ws_bytes) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!q || !k_ctx || !v_ctx || !k_tree || !v_tree || !lens || !node_count || !tree_mask || !out)
+    return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || T_max < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || !std::isfinite(scale) ||
+      !(scale > 0.f))
+    return ADAPLD_ERR_INVALID_ARG;
+  if (D != ADAPLD_HEAD_DIM || T_max > ADAPLD_MAX_TREE_NODES) return ADAPLD_ERR_UNSUPPORTED;
+  if (misaligned16(q) || misaligned16(k_ctx) || misaligned16(v_ctx) || misaligned16(k_tree) ||
+      misaligned16(v_tree) || misaligned16(out))
+    return ADAPLD_ERR_INVALID_ARG;
+  const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
+  const size_t need = adapld::verify_ws_bytes(p, B, Hkv);
+  if (need > 0 && !ws) return ADAPLD_ERR_NULL_ARG;
+  if (ws_bytes < need) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  if (need > 0 && misaligned16(ws)) return ADAPLD_ERR_INVALID_ARG;
+  return ADAPLD_OK;
+}
 
 }  // namespace
 
@@ -60,6 +134,13 @@ size_t adapld_workspace_bytes(int op, int B, int L_stride, int d, int k, int T_m
     case ADAPLD_OP_BUILD_DRAFT_TREE_PAPER:   // k carries W
       if (k < 1 || k > 64 || d < 8 || d % 8 || (int64_t)B * k > ADAPLD_MAX_SEMANTIC_BATCH) return 0;
       return adapld::paper_tree_ws_bytes(B, L_stride, k, d);
+    case ADAPLD_OP_STEP: {
+      if (k < 1 || k > ADAPLD_MAX_K || T_max < 1 || T_max > ADAPLD_MAX_TREE_NODES || Hq < 1 || Hkv < 1 ||
+          Hq % Hkv)
+        return 0;
+      const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
+      return step_sem_part(B, L_stride, k) + adapld::verify_ws_bytes(p, B, Hkv);
+    }
     case ADAPLD_OP_TREE_VERIFY_ATTN: {
       if (T_max < 1 || T_max > ADAPLD_MAX_TREE_NODES || Hq < 1 || Hkv < 1 || Hq % Hkv) return 0;
       const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
@@ -87,11 +168,9 @@ int adapld_verify_plan(int B, int L_stride, int T_max, int Hq, int Hkv, int32_t*
 int adapld_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
                          int32_t* cand_pos, int32_t* cand_count, int32_t* match_n,
                          hipStream_t stream) {
-  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
-  if (B == 0) return ADAPLD_OK;
-  if (!tokens || !lens || !cand_pos || !cand_count || !match_n) return ADAPLD_ERR_NULL_ARG;
-  if (L_stride < 1) return ADAPLD_ERR_INVALID_ARG;
-  if (n_max < 1 || n_max > ADAPLD_MAX_NMAX) return ADAPLD_ERR_UNSUPPORTED;
+  if (const int st = check_lexical(tokens, lens, B, L_stride, n_max, cand_pos, cand_count, match_n);
+      st != ADAPLD_OK || B == 0)
+    return st;
   return hip_status(adapld::launch_lexical_match(tokens, lens, B, L_stride, n_max, cand_pos,
                                                  cand_count, match_n, stream));
 }
@@ -101,17 +180,10 @@ int adapld_semantic_topk(const uint16_t* bank, const uint16_t* query, const int3
                          int d, int k, float tau, int32_t* topk_pos, float* topk_score,
                          int32_t* topk_count, int32_t* kind, void* ws, size_t ws_bytes,
                          hipStream_t stream) {
-  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
-  if (B == 0) return ADAPLD_OK;
-  if (!bank || !lens || !cand_pos || !cand_count || !topk_pos || !topk_score || !topk_count ||
-      !kind || !ws)
-    return ADAPLD_ERR_NULL_ARG;
-  if (L_stride < 1 || d < 8 || d % 8 != 0 || k < 1) return ADAPLD_ERR_INVALID_ARG;
-  if (d > ADAPLD_MAX_HIDDEN || k > ADAPLD_MAX_K || B > ADAPLD_MAX_SEMANTIC_BATCH ||
-      (int64_t)B * L_stride > INT32_MAX)
-    return ADAPLD_ERR_UNSUPPORTED;
-  if (misaligned16(bank) || (query && misaligned16(query))) return ADAPLD_ERR_INVALID_ARG;
-  if (ws_bytes < semantic_ws(B, L_stride, k)) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  if (const int st = check_semantic(bank, query, lens, cand_pos, cand_count, B, L_stride, d, k,
+                                    tau, topk_pos, topk_score, topk_count, kind, ws, ws_bytes);
+      st != ADAPLD_OK || B == 0)
+    return st;
   return hip_status(adapld::launch_semantic_topk(bank, query, lens, cand_pos, cand_count, B,
                                                  L_stride, d, k, tau, topk_pos, topk_score,
                                                  topk_count, kind, static_cast<uint64_t*>(ws),
@@ -152,14 +224,11 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
                             int k, int W, int S, int T_max, int32_t* node_token,
                             int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
                             int32_t* node_count, uint64_t* tree_mask, hipStream_t stream) {
-  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
-  if (B == 0) return ADAPLD_OK;
-  if (!tokens || !lens || !topk_pos || !topk_count || !kind || !node_token || !node_parent ||
-      !node_depth || !node_src || !node_count || !tree_mask)
-    return ADAPLD_ERR_NULL_ARG;
-  if (L_stride < 1 || k < 1 || W < 1 || S < 0 || T_max < 1) return ADAPLD_ERR_INVALID_ARG;
-  if (k > ADAPLD_MAX_K || T_max > ADAPLD_MAX_TREE_NODES) return ADAPLD_ERR_UNSUPPORTED;
-  if ((long long)W * (S + 1LL) > T_max) return ADAPLD_ERR_INVALID_ARG;
+  if (const int st = check_tree(tokens, lens, topk_pos, topk_count, kind, B, L_stride, k, W, S,
+                                T_max, node_token, node_parent, node_depth, node_src, node_count,
+                                tree_mask);
+      st != ADAPLD_OK || B == 0)
+    return st;
   return hip_status(adapld::launch_build_draft_tree(tokens, lens, topk_pos, topk_count, kind, B,
                                                     L_stride, k, W, S, T_max, node_token,
                                                     node_parent, node_depth, node_src, node_count,
@@ -197,25 +266,61 @@ int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint
                             int L_stride, int T_max, int Hq, int Hkv, int D, float scale,
                             uint16_t* out, float* lse, void* ws, size_t ws_bytes,
                             hipStream_t stream) {
-  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
-  if (B == 0) return ADAPLD_OK;
-  if (!q || !k_ctx || !v_ctx || !k_tree || !v_tree || !lens || !node_count || !tree_mask || !out)
-    return ADAPLD_ERR_NULL_ARG;
-  if (L_stride < 1 || T_max < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || !std::isfinite(scale) ||
-      !(scale > 0.f))
-    return ADAPLD_ERR_INVALID_ARG;
-  if (D != ADAPLD_HEAD_DIM || T_max > ADAPLD_MAX_TREE_NODES) return ADAPLD_ERR_UNSUPPORTED;
-  if (misaligned16(q) || misaligned16(k_ctx) || misaligned16(v_ctx) || misaligned16(k_tree) ||
-      misaligned16(v_tree) || misaligned16(out))
-    return ADAPLD_ERR_INVALID_ARG;
+  if (const int st = check_verify(q, k_ctx, v_ctx, k_tree, v_tree, lens, node_count, tree_mask, B,
+                                  L_stride, T_max, Hq, Hkv, D, scale, out, lse, ws, ws_bytes);
+      st != ADAPLD_OK || B == 0)
+    return st;
   const adapld::VerifyPlan p = adapld::plan_verify(B, L_stride, T_max, Hq, Hkv);
-  const size_t need = adapld::verify_ws_bytes(p, B, Hkv);
-  if (need > 0 && !ws) return ADAPLD_ERR_NULL_ARG;
-  if (ws_bytes < need) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
-  if (need > 0 && misaligned16(ws)) return ADAPLD_ERR_INVALID_ARG;
   return hip_status(adapld::launch_tree_verify_attn(q, k_ctx, v_ctx, k_tree, v_tree, lens,
                                                     node_count, tree_mask, B, L_stride, T_max, Hq,
                                                     Hkv, scale, out, lse, ws, p, stream));
+}
+
+int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank, const uint16_t* query,
+                const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx, const uint16_t* k_tree,
+                const uint16_t* v_tree, int B, int L_stride, int d, int n_max, int k, int W, int S,
+                int T_max, int Hq, int Hkv, int D, float tau, float scale, int32_t* cand_pos,
+                int32_t* cand_count, int32_t* match_n, int32_t* topk_pos, float* topk_score,
+                int32_t* topk_count, int32_t* kind, int32_t* node_token, int32_t* node_parent,
+                int32_t* node_depth, int32_t* node_src, int32_t* node_count, uint64_t* tree_mask,
+                uint16_t* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!ws) return ADAPLD_ERR_NULL_ARG;
+  if (misaligned16(ws)) return ADAPLD_ERR_INVALID_ARG;
+  if (k < 1 || L_stride < 1) return ADAPLD_ERR_INVALID_ARG;
+  if (k > ADAPLD_MAX_K) return ADAPLD_ERR_UNSUPPORTED;
+  const size_t sem = step_sem_part(B, L_stride, k);
+  if (ws_bytes < sem) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  void* ws_ver = static_cast<char*>(ws) + sem;
+  const size_t ver_bytes = ws_bytes - sem;
+  // Every call is validated before the first is enqueued.
+  int st = check_lexical(tokens, lens, B, L_stride, n_max, cand_pos, cand_count, match_n);
+  if (st == ADAPLD_OK)
+    st = check_semantic(bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, tau, topk_pos,
+                        topk_score, topk_count, kind, ws, sem);
+  if (st == ADAPLD_OK)
+    st = check_tree(tokens, lens, topk_pos, topk_count, kind, B, L_stride, k, W, S, T_max, node_token,
+                    node_parent, node_depth, node_src, node_count, tree_mask);
+  if (st == ADAPLD_OK)
+    st = check_verify(q, k_ctx, v_ctx, k_tree, v_tree, lens, node_count, tree_mask, B, L_stride, T_max,
+                      Hq, Hkv, D, scale, out, lse, ws_ver, ver_bytes);
+  if (st != ADAPLD_OK) return st;
+  hipError_t e = adapld::launch_lexical_match(tokens, lens, B, L_stride, n_max, cand_pos, cand_count,
+                                              match_n, stream);
+  if (e == hipSuccess)
+    e = adapld::launch_semantic_topk(bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, tau,
+                                     topk_pos, topk_score, topk_count, kind, static_cast<uint64_t*>(ws),
+                                     nullptr, 0, stream);
+  if (e == hipSuccess)
+    e = adapld::launch_build_draft_tree(tokens, lens, topk_pos, topk_count, kind, B, L_stride, k, W, S,
+                                        T_max, node_token, node_parent, node_depth, node_src, node_count,
+                                        tree_mask, stream);
+  if (e == hipSuccess)
+    e = adapld::launch_tree_verify_attn(q, k_ctx, v_ctx, k_tree, v_tree, lens, node_count, tree_mask, B,
+                                        L_stride, T_max, Hq, Hkv, scale, out, lse, ws_ver,
+                                        adapld::plan_verify(B, L_stride, T_max, Hq, Hkv), stream);
+  return hip_status(e);
 }
 
 int adapld_accept_greedy(const int32_t* node_token, const int32_t* node_parent,

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     for n in names:
         assert hasattr(lib, n), n
         assert n in binding.SIGNATURES, n
@@ -96,6 +96,37 @@ def test_embed_validation(lib):
     need = lib.adapld_workspace_bytes(5, 2, 64, 128, 8, 0, 0, 0, 0)
     assert need >= lib.adapld_workspace_bytes(2, 2, 64, 128, 8, 0, 0, 0, 0) + 2 * 64 * 5
     assert f(*args(ws_bytes=need - 1)) == WS_SMALL
+
+
+def test_step_validation(lib):
+    f = lib.adapld_step
+    nan = float("nan")
+    args = lambda **kw: [kw.get(n, v) for n, v in (  # noqa: E731
+        ("tokens", P), ("lens", P), ("bank", P), ("query", N), ("q", P), ("k_ctx", P), ("v_ctx", P),
+        ("k_tree", P), ("v_tree", P), ("B", 2), ("L_stride", 64), ("d", 128), ("n_max", 3), ("k", 8),
+        ("W", 4), ("S", 4), ("T_max", 20), ("Hq", 8), ("Hkv", 2), ("D", 128), ("tau", nan), ("scale", 0.1),
+        *[(f"o{i}", P) for i in range(15)], ("ws", P), ("ws_bytes", 1 << 30), ("stream", N))]
+    assert f(*args(B=0)) == OK
+    assert f(*args(B=-1)) == INVALID
+    assert f(*args(ws=N)) == NULL
+    assert f(*args(ws=ctypes.c_void_p(0x10008))) == INVALID
+    assert f(*args(tokens=N)) == NULL                 # the lexical call's check
+    assert f(*args(n_max=65)) == UNSUPPORTED
+    assert f(*args(d=12)) == INVALID                  # the rerank's
+    assert f(*args(bank=ctypes.c_void_p(0x10008))) == INVALID
+    assert f(*args(W=0)) == INVALID                   # the tree's
+    assert f(*args(T_max=19)) == INVALID              # below W*(S+1)
+    assert f(*args(D=64)) == UNSUPPORTED              # the verify's
+    assert f(*args(scale=0.0)) == INVALID
+    assert f(*args(Hq=6, Hkv=4)) == INVALID
+    need = lib.adapld_workspace_bytes(7, 2, 64, 128, 8, 20, 8, 2, 128)
+    sem = lib.adapld_workspace_bytes(2, 2, 64, 128, 8, 0, 0, 0, 0)
+    ver = lib.adapld_workspace_bytes(4, 2, 64, 0, 0, 20, 8, 2, 128)
+    assert need == (sem + 255) // 256 * 256 + ver
+    assert f(*args(ws_bytes=(sem + 255) // 256 * 256 - 1)) == WS_SMALL
+    split = lib.adapld_workspace_bytes(7, 1, 4096, 128, 8, 20, 8, 2, 128)   # a split verify: partials too
+    assert split > lib.adapld_workspace_bytes(2, 1, 4096, 128, 8, 0, 0, 0, 0) + 255
+    assert f(*args(B=1, L_stride=4096, T_max=20, ws_bytes=split - 1)) == WS_SMALL
 
 
 def test_paper_tree_validation(lib):
