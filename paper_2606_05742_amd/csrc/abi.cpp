@@ -308,14 +308,14 @@ int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank
   if (st != ADAPLD_OK) return st;
   hipError_t e = adapld::launch_lexical_match(tokens, lens, B, L_stride, n_max, cand_pos, cand_count,
                                               match_n, stream);
+  // The rerank's merge kernel builds the tree right after ranking (the same
+  // wave routine as adapld_build_draft_tree), which saves that launch.
+  const adapld::TreeOut tree{tokens, W, S, T_max, node_token, node_parent, node_depth, node_src, node_count,
+                             tree_mask};
   if (e == hipSuccess)
     e = adapld::launch_semantic_topk(bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, tau,
                                      topk_pos, topk_score, topk_count, kind, static_cast<uint64_t*>(ws),
-                                     nullptr, 0, stream);
-  if (e == hipSuccess)
-    e = adapld::launch_build_draft_tree(tokens, lens, topk_pos, topk_count, kind, B, L_stride, k, W, S,
-                                        T_max, node_token, node_parent, node_depth, node_src, node_count,
-                                        tree_mask, stream);
+                                     nullptr, 0, stream, 1, &tree);
   if (e == hipSuccess)
     e = adapld::launch_tree_verify_attn(q, k_ctx, v_ctx, k_tree, v_tree, lens, node_count, tree_mask, B,
                                         L_stride, T_max, Hq, Hkv, scale, out, lse, ws_ver,

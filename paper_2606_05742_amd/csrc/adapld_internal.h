@@ -51,12 +51,26 @@ hipError_t launch_lexical_match(const int32_t* tokens, const int32_t* lens, int 
                                 int n_max, int32_t* cand_pos, int32_t* cand_count,
                                 int32_t* match_n, hipStream_t stream);
 
+// Where a draft tree is written (the layouts of adapld_build_draft_tree).
+struct TreeOut {
+  const int32_t* tokens;   // [B, L_stride]
+  int W, S, T_max;
+  int32_t* node_token;
+  int32_t* node_parent;
+  int32_t* node_depth;
+  int32_t* node_src;
+  int32_t* node_count;
+  uint64_t* tree_mask;
+};
+
+// With `tree`, the merge kernel also builds each sequence's draft tree from
+// the ranked list it has just formed (the step's fused rank + tree).
 hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
                                 const int32_t* cand_pos, const int32_t* cand_count, int B,
                                 int L_stride, int d, int k, float tau, int32_t* topk_pos,
                                 float* topk_score, int32_t* topk_count, int32_t* kind,
                                 uint64_t* ws_keys, const int32_t* cand_kind, int rerank_only,
-                                hipStream_t stream, int seq_div = 1);
+                                hipStream_t stream, int seq_div = 1, const TreeOut* tree = nullptr);
 
 hipError_t launch_build_draft_tree(const int32_t* tokens, const int32_t* lens,
                                    const int32_t* topk_pos, const int32_t* topk_count,

@@ -25,6 +25,7 @@
 // the kind.
 #include "adapld_internal.h"
 #include "device_utils.h"
+#include "tree_device.h"
 
 namespace adapld {
 namespace {
@@ -292,8 +293,10 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
                                                                   int32_t* __restrict__ topk_pos,
                                                                   float* __restrict__ topk_score,
                                                                   int32_t* __restrict__ topk_count,
-                                                                  int32_t* __restrict__ kind) {
+                                                                  int32_t* __restrict__ kind,
+                                                                  const TreeOut tree) {
   __shared__ uint64_t s_cand[kMaxCand];
+  __shared__ int s_start[ADAPLD_MAX_TREE_NODES];
   __shared__ uint64_t s_red[kScanWaves];
   __shared__ int s_sum[kScanWaves][2];
   __shared__ int s_ncand;
@@ -389,6 +392,8 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
     kind[b] = cc > 0 ? (a.cand_kind ? a.cand_kind[b] : ADAPLD_KIND_LEX)
                      : (count > 0 ? ADAPLD_KIND_SEM : ADAPLD_KIND_NONE);
   }
+  // The step's tree, from the ranked list in registers (kind NONE has count 0).
+  if (tree.tokens) build_tree_wave(tree, b, a.L_stride, L, keep ? key_pos(mine) : -1, count, s_start);
 }
 
 template <int NIT>
@@ -404,7 +409,7 @@ hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, con
                                 int L_stride, int d, int k, float tau, int32_t* topk_pos,
                                 float* topk_score, int32_t* topk_count, int32_t* kind,
                                 uint64_t* ws_keys, const int32_t* cand_kind, int rerank_only,
-                                hipStream_t stream, int seq_div) {
+                                hipStream_t stream, int seq_div, const TreeOut* tree) {
   ScanArgs a{bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, scan_lists(L_stride), ws_keys,
              cand_kind, rerank_only, seq_div};
   const int nit = (d + 8 * kWave - 1) / (8 * kWave);
@@ -423,8 +428,9 @@ hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, con
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const TreeOut t = tree ? *tree : TreeOut{};
   hipLaunchKernelGGL(topk_merge_kernel, dim3(B), dim3(kScanThreads), 0, stream, a, tau, topk_pos,
-                     topk_score, topk_count, kind);
+                     topk_score, topk_count, kind, t);
   return hipGetLastError();
 }
 

@@ -1,0 +1,81 @@
+// The draft tree of one sequence from its ranked list (Sec. 3.5 reuse
+// construction organised as a draft tree, Sec. 3.6), built by one wave.
+// Used by the tree kernel and by the rerank's merge kernel when the step asks
+// it to build the tree right after ranking.
+//
+// Lane i holds ranked entry r (i < cnt): its successor token M[r+1] opens a
+// branch unless a lower lane already holds that token; ballots number the
+// branches and keep the first W.  A wave prefix sum of the branch lengths
+// gives each branch its node offset, so every node, its parent link and its
+// ancestor bits are written without serial dependence.  Because every branch
+// is a chain, the ancestor-or-self set of node u is the contiguous node range
+// [start of u's branch, u], which is how the mask rows are filled.
+#pragma once
+
+#include "adapld_internal.h"
+#include "device_utils.h"
+
+namespace adapld {
+
+
+// Called by every lane of one wave; s_start holds ADAPLD_MAX_TREE_NODES ints
+// of LDS that only this wave uses.
+__device__ __forceinline__ void build_tree_wave(const TreeOut& t, int b, int L_stride, int L, int r, int cnt,
+                                                int* s_start) {
+  const int lane = lane_id();
+  const int32_t* __restrict__ M = t.tokens + (size_t)b * L_stride;
+  int tok = -1;
+  const bool valid = lane < cnt && r >= 0 && r <= L - 2;
+  if (valid) tok = M[r + 1];
+  // A lane is a new branch if no lower valid lane holds the same successor token.
+  bool dup = false;
+  for (int j = 0; j < cnt; ++j) {   // lane j's token and validity as scalars
+    const int tj = __builtin_amdgcn_readlane(tok, j);
+    const int vj = __builtin_amdgcn_readlane((int)valid, j);
+    dup |= (j < lane) && vj && tj == tok;
+  }
+  const bool opens = valid && !dup;
+  const int branch = __popcll(__ballot(opens) & lanes_below());
+  const bool keep = opens && branch < t.W;
+  const int len = keep ? min(t.S + 1, L - 1 - r) : 0;
+
+  // Exclusive prefix sum of branch lengths over lanes (branch order = lane order).
+  const int incl = wave_incl_scan_i32(len);
+  const int start = incl - len;
+  const int T = __builtin_amdgcn_readlane(incl, kWave - 1);
+
+  const size_t nb = (size_t)b * t.T_max;
+  for (int dd = 0; dd < len; ++dd) {
+    const int u = start + dd;
+    t.node_token[nb + u] = M[r + 1 + dd];
+    t.node_parent[nb + u] = dd == 0 ? -1 : u - 1;
+    t.node_depth[nb + u] = dd;
+    t.node_src[nb + u] = r + 1 + dd;
+    s_start[u] = start;
+  }
+  if (lane == 0) t.node_count[b] = T;
+  // s_start is written and read by this wave only; its LDS operations
+  // complete in order, so a wave-level fence is enough.
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+  const int nw = (t.T_max + 63) / 64;
+  uint64_t* __restrict__ mrow = t.tree_mask + nb * nw;
+  for (int idx = lane; idx < t.T_max * nw; idx += kWave) {
+    const int u = idx / nw;
+    const int w = idx - u * nw;
+    uint64_t bits = 0;
+    if (u < T) {
+      const int lo = max(s_start[u], 64 * w);
+      const int hi = min(u, 64 * w + 63);  // inclusive
+      if (lo <= hi) {
+        const int n = hi - lo + 1;
+        bits = (n == 64 ? ~0ull : ((1ull << n) - 1)) << (lo - 64 * w);
+      }
+    }
+    mrow[idx] = bits;
+  }
+}
+
+}  // namespace adapld
