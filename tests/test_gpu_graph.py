@@ -1,4 +1,5 @@
-"""The four-call step captured in a HIP graph and replayed.
+"""The step captured in a HIP graph and replayed, both as four entry-point
+calls and as one adapld_step call.
 
 Every replay must reproduce the eager step bit for bit, also with other eager
 work (a different batch through the same buffers) and host synchronisations
@@ -36,6 +37,12 @@ def _run(cfg, bufs, d):
                             ws=bufs.ws_ver)
 
 
+def _run_native(cfg, bufs, d):
+    # adapld.step: one adapld_step call on the current stream (the capture
+    # stream while capturing)
+    adapld.step(*d, n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, buffers=bufs)
+
+
 def _snapshot(bufs):
     return {n: getattr(bufs, n).clone() for n in OUTPUTS}
 
@@ -50,21 +57,23 @@ def _poison(bufs):
             t.fill_(-7 if t.dtype != torch.uint64 else 0)
 
 
+@pytest.mark.parametrize("native", [False, True])
 @pytest.mark.parametrize("L", [700, 3000])
-def test_graph_replay_matches_eager(L):
+def test_graph_replay_matches_eager(L, native):
     # L = 3000 with B = 2 splits the verify context (the combine kernel runs too).
     cfg = small_config(B=2, L=L, d=512, Hq=8, Hkv=2, k=8, W=4, S=6, n_max=3, seed=97, forced_every=2)
     other = small_config(B=2, L=L, d=512, Hq=8, Hkv=2, k=8, W=4, S=6, n_max=3, seed=98, forced_every=2)
     d = _upload(make_inputs(cfg))
     d_other = _upload(make_inputs(other))
     bufs = adapld.StepBuffers.allocate(cfg.B, cfg.L, cfg.d, cfg.k, cfg.T_max, cfg.Hq, cfg.Hkv, cfg.D)
+    run = _run_native if native else _run
 
     _poison(bufs)
-    _run(cfg, bufs, d)
+    run(cfg, bufs, d)
     torch.cuda.synchronize()
     ref = _snapshot(bufs)
     _poison(bufs)
-    _run(other, bufs, d_other)
+    run(other, bufs, d_other)
     torch.cuda.synchronize()
     ref_other = _snapshot(bufs)
     assert not torch.equal(ref["out"], ref_other["out"])
@@ -74,7 +83,7 @@ def test_graph_replay_matches_eager(L):
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.stream(side):
         with torch.cuda.graph(graph, stream=side):
-            _run(cfg, bufs, d)
+            run(cfg, bufs, d)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
 
@@ -87,7 +96,7 @@ def test_graph_replay_matches_eager(L):
             assert torch.equal(got[n], ref[n]), f"replay {rep}: {n} differs from the eager step"
         # eager work on another batch through the same buffers between replays
         _poison(bufs)
-        _run(other, bufs, d_other)
+        run(other, bufs, d_other)
         torch.cuda.synchronize()
         for n in ("out", "lse", "node_count"):
             assert torch.equal(getattr(bufs, n), ref_other[n]), f"eager step after replay {rep}: {n}"
