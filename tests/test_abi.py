@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(lib):
 def test_status_strings(lib):
     for code in (OK, NULL, INVALID, UNSUPPORTED, WS_SMALL, -5, 123):
         assert lib.adapld_status_string(code)
-    assert lib.adapld_version() == 10000
+    assert lib.adapld_version() == 10100
     assert lib.adapld_last_hip_error() == 0
 
 
