@@ -24,13 +24,43 @@ constexpr int kLexChunk = 32768;   // tokens per LDS piece (128 KiB)
 constexpr int kHalo = kMaxNmax;    // >= n_max - 1, multiple of 4
 
 // Stage tokens [lo, hi) at s_tok[kHalo - (p0 - lo) ...]: s_tok[kHalo + i] holds M[p0 + i].
+// A piece holds at most kLexChunk + kHalo tokens.  On the 16-byte path every
+// load of a thread is issued before the first LDS write, so the loads are in
+// flight together instead of one round trip per loop iteration: R (the
+// number of int4 per thread the piece needs) is a compile-time count, indices
+// are clamped into the piece, and a clamped slot writes the last element
+// again with the value it already holds, so neither loads nor writes need a
+// branch (a guarded write would let the compiler sink its load behind it).
+constexpr int kStageVec = (kLexChunk + kHalo) / 4 / kLexThreads + 1;
+template <int R>
+__device__ __forceinline__ void stage_vec(const int4* __restrict__ src, int* dst, int n4) {
+  const int tid = threadIdx.x;
+  int4 v[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) v[r] = src[min(tid + r * kLexThreads, n4 - 1)];
+#pragma unroll
+  for (int r = 0; r < R; ++r) *reinterpret_cast<int4*>(&dst[4 * min(tid + r * kLexThreads, n4 - 1)]) = v[r];
+}
 __device__ __forceinline__ void stage(const int32_t* __restrict__ M, int* s_tok, int p0, int lo, int hi) {
   const int base = kHalo - (p0 - lo);  // LDS slot of token lo
   const int n = hi - lo;
   if (((lo | base) & 3) == 0 && (reinterpret_cast<uintptr_t>(M + lo) & 15) == 0) {
     const int n4 = n >> 2;
-    for (int i = threadIdx.x; i < n4; i += kLexThreads)
-      *reinterpret_cast<int4*>(&s_tok[base + 4 * i]) = *reinterpret_cast<const int4*>(M + lo + 4 * i);
+    const int4* __restrict__ src = reinterpret_cast<const int4*>(M + lo);
+    int* dst = s_tok + base;
+    static_assert(kStageVec == 9, "one case per count");
+    switch ((n4 + kLexThreads - 1) / kLexThreads) {
+      case 0: break;
+      case 1: stage_vec<1>(src, dst, n4); break;
+      case 2: stage_vec<2>(src, dst, n4); break;
+      case 3: stage_vec<3>(src, dst, n4); break;
+      case 4: stage_vec<4>(src, dst, n4); break;
+      case 5: stage_vec<5>(src, dst, n4); break;
+      case 6: stage_vec<6>(src, dst, n4); break;
+      case 7: stage_vec<7>(src, dst, n4); break;
+      case 8: stage_vec<8>(src, dst, n4); break;
+      default: stage_vec<9>(src, dst, n4); break;
+    }
     for (int i = 4 * n4 + threadIdx.x; i < n; i += kLexThreads) s_tok[base + i] = M[lo + i];
   } else {
     for (int i = threadIdx.x; i < n; i += kLexThreads) s_tok[base + i] = M[lo + i];
