@@ -111,9 +111,11 @@ def run(x, cfg, top, W, S, T_max=None, seqs=None, dense_bank=True, ctx=""):
 
 
 # L = 701 and 1503 give rows that do not start on 16 bytes (token-at-a-time
-# loads); 9001 and 20000 take several passes of the setup kernel.
+# loads); 9001 and 20000 take several passes of the setup kernel; W = 64 (the
+# limit) fills every lane of the setup and assembly waves.
 @pytest.mark.parametrize("L,d,W,S,seed", [(300, 128, 4, 12, 1), (2100, 256, 8, 6, 2), (701, 520, 1, 0, 3),
-                                          (1503, 128, 16, 3, 4), (9001, 64, 4, 12, 5), (20000, 64, 8, 4, 6)])
+                                          (1503, 128, 16, 3, 4), (9001, 64, 4, 12, 5), (20000, 64, 8, 4, 6),
+                                          (900, 64, 64, 20, 7)])
 def test_paper_tree(L, d, W, S, seed):
     cfg = small_config(B=6, L=L, d=d, k=8, n_max=3, seed=200 + seed, V=40, forced_every=3)
     x = make_inputs(cfg, with_verify=False)
