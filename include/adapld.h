@@ -302,6 +302,10 @@ int adapld_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, co
  * z = scale * q . key (fp32 accumulation of bf16 products):
  *   out[b, u, h] = softmax(z) . values        (bf16)
  *   lse[b, h, u] = ln sum exp(z)              (fp32)
+ * A row whose mask row is empty attends to the context keys only: that is how
+ * the root (the last context token, whose K/V are already cached at L-1) is
+ * verified with its tree in one call, as row 0 with the tree's rows and mask
+ * bits shifted by one.
  *
  *   q          bf16 [B, T_max, Hq, D]
  *   k_ctx      bf16 [B, Hkv, L_stride, D]
