@@ -30,7 +30,7 @@
  *
  *   5. adapld_accept_greedy     greedy acceptance of the tree and compaction
  *                               of the accepted nodes' K/V (Sec. 3.6,
- *                               Appendix A)
+ *                               Appendix C)
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -369,7 +369,7 @@ int adapld_semantic_topk_embed(const uint16_t* bank, const uint16_t* query, cons
 
 /*
  * adapld_accept_greedy -- greedy verification of the draft tree (Sec. 3.6:
- * verification follows the standard speculative-decoding rule; Appendix A:
+ * verification follows the standard speculative-decoding rule; Appendix C:
  * with greedy decoding a draft token is kept when it equals the target's own
  * choice, and the first mismatch ends it) and compaction of the kept nodes'
  * K/V into the cache.

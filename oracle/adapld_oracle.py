@@ -22,7 +22,8 @@ Four steps, per sequence, in the paper's order (Sec. 3.3 - 3.6, Algorithm 1):
                        Algorithm 1): the main copy path of a lexical anchor,
                        branch tokens from the target's top tokens after the
                        anchor, and one successor token per branch retrieved
-                       by a lexical match of the branch token and a
+                       by a lexical match of the branch token (with the
+                       token-embedding backoff when it never occurs) and a
                        hidden-state rerank against the anchor.
 ``tree_verify_attn``-- tree-masked attention over the KV cache (Sec. 3.6,
                        tree attention after Medusa), softmax in float64.
@@ -31,7 +32,7 @@ Four steps, per sequence, in the paper's order (Sec. 3.3 - 3.6, Algorithm 1):
                        lexical miss, every earlier position whose token
                        embedding has cosine >= tau with the last token's.
 ``accept_greedy``   -- greedy verification of the tree (Sec. 3.6 and the
-                       speculative-decoding background of Appendix A: with
+                       speculative-decoding background of Appendix C: with
                        greedy decoding a draft token is kept when it equals
                        the target's own choice, up to the first mismatch),
                        and ``compact_kv`` -- the accepted nodes' K/V moved to
@@ -63,11 +64,16 @@ reproduced workload differs from its text):
   l = min(S+1, L-1-j*); the branch tokens are the given top tokens after the
   anchor in their order, without negatives, repeats and (lexical hit) the
   main path's first token, at most W of them; a branch token b gets the
-  successor M[t*+1] where t* maximises cos(H[t-1], H[j*]) over the positions
-  t in [1, L-2] with M_t = b (lowest t among equal scores); a token with no
-  such position gets no successor (the token-embedding fallback is not
-  applied to successors); nodes: the main path as a chain, then each branch
-  token (depth 0) followed by its successor (depth 1);
+  successor M[t*+1] where t* maximises cos(H[t-1], H[j*]) over its
+  candidate positions t in [1, L-2] (lowest t among equal scores): those
+  with M_t = b, or, when b never occurs there and an embedding table is
+  given, those whose token embedding has cosine >= tau with b's (the
+  lexical-first backoff of Sec. 3.3 with b as the query); a token with no
+  candidate gets no successor; whether a lexical anchor's branches get
+  successors is an argument, since the text of Sec. 3.5 drafts them for
+  every branch and Algorithm 1 only after a semantic hit; nodes: the main
+  path as a chain, then each branch token (depth 0) followed by its
+  successor (depth 1);
 * the token-embedding fallback scores positions j in [0, L-2] (the paper's
   1 <= j < |M|, 1-based) by cos(e[M_j], e[M_{L-1}]) (a zero norm gives 0),
   keeps those >= tau in ascending order, and is used only when the lexical
@@ -254,12 +260,47 @@ def build_draft_tree(tokens: np.ndarray, kind: int, ranked, W: int, S: int):
                 branches=branches, mask=mask)
 
 
-def build_draft_tree_paper(tokens: np.ndarray, bank: np.ndarray, kind: int, ranked, top_tokens, W: int, S: int):
+SUCC_EVERY_BRANCH = 0    # Sec. 3.5 text: successor drafting for every branch token
+SUCC_SEMANTIC_ONLY = 1   # Algorithm 1: no successors when the anchor is a lexical hit
+
+
+def successor_candidates(tokens: np.ndarray, b: int, emb=None, tau=None):
+    """The candidate set of a branch token used as a secondary query (Sec. 3.5,
+    successor drafting, with the lexical-first backoff rule of Sec. 3.3).
+
+    Positions t in [1, L-2] (a preceding hidden state and a following token).
+    Lexical set: M_t == b.  When it is empty and an embedding table is given,
+    the semantic set instead: cos(emb[M_t], emb[b]) >= tau (a token id outside
+    the table has a zero embedding, cosine 0).  Returns the positions,
+    ascending.
+    """
+    M = np.asarray(tokens)
+    L = int(M.shape[0])
+    ts = list(range(1, L - 1))
+    C = [t for t in ts if int(M[t]) == b]
+    if C or emb is None or not ts:
+        return C
+    V, d = emb.shape
+    def row(tok):
+        return emb[tok] if 0 <= tok < V else np.zeros(d)
+    E = np.stack([row(int(M[t])) for t in ts])
+    s = cosine_rows(E, np.arange(len(ts)), row(b))
+    return [t for i, t in enumerate(ts) if s[i] >= tau]
+
+
+def build_draft_tree_paper(tokens: np.ndarray, bank: np.ndarray, kind: int, ranked, top_tokens, W: int, S: int,
+                           succ_mode: int = SUCC_EVERY_BRANCH, emb=None, tau=None):
     """The paper's draft construction (Sec. 3.5, Eqs. (8)-(15); Algorithm 1).
 
     tokens: (L,) ints; bank: (L, d) float64 hidden states; kind and ranked:
     the retrieval outcome (ranked positions, best first); top_tokens: the
     target's top tokens after the anchor j* = ranked[0], best first.
+    succ_mode: SUCC_EVERY_BRANCH drafts a successor for every branch token
+    (the text of Sec. 3.5); SUCC_SEMANTIC_ONLY only when the anchor came from
+    the semantic fallback (Algorithm 1 leaves d_succ empty in its strict
+    branch).  emb, tau: the token-embedding table (V, d) and threshold of the
+    successor retrieval's semantic backoff; None keeps successor retrieval
+    lexical only.
     Returns the same dict as build_draft_tree; src is the memory position a
     node copies, or -1 for a branch token (it comes from the model).
     """
@@ -283,13 +324,14 @@ def build_draft_tree_paper(tokens: np.ndarray, bank: np.ndarray, kind: int, rank
             branches.append(b)
             if len(branches) == W:
                 break
+        drafts_successors = succ_mode == SUCC_EVERY_BRANCH or kind == KIND_SEM
         for b in branches:
             u = len(token)
             token.append(b)
             parent.append(-1)
             depth.append(0)
             src.append(-1)
-            C = [t for t in range(1, L - 1) if int(M[t]) == b]
+            C = successor_candidates(M, b, emb, tau) if drafts_successors else []
             if C:
                 s_b = cosine_rows(bank, [t - 1 for t in C], bank[j])
                 best = C[int(np.argmax(s_b))]   # first maximum: the lowest t
@@ -343,7 +385,7 @@ def tree_verify_attn(Q, Kc, Vc, Kt, Vt, mask, L: int, scale: float):
 
 
 # --------------------------------------------------------------------------
-# Step 5: greedy acceptance and KV compaction (Sec. 3.6; Appendix A)
+# Step 5: greedy acceptance and KV compaction (Sec. 3.6; Appendix C)
 # --------------------------------------------------------------------------
 
 def accept_greedy(token, parent, root_next: int, node_next):

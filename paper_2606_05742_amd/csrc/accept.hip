@@ -1,6 +1,6 @@
 // Greedy acceptance of the draft tree (Sec. 3.6: verification follows the
 // standard speculative-decoding rule, which with greedy decoding keeps a draft
-// token when it equals the target's own choice, Appendix A) and compaction of
+// token when it equals the target's own choice, Appendix C) and compaction of
 // the accepted nodes' K/V into the cache.
 //
 // One workgroup of 256 threads per sequence, thread u for node u (T_max is at

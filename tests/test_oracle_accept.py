@@ -1,5 +1,5 @@
 """Pins of the oracle's greedy acceptance and KV compaction (Sec. 3.6;
-Appendix A: with greedy decoding a draft token is kept when it equals the
+Appendix C: with greedy decoding a draft token is kept when it equals the
 target's own choice, and the first mismatch ends verification).
 
 The central pin is the property the paper relies on: the tokens a step emits

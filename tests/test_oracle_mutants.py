@@ -14,7 +14,7 @@ from concurrent.futures import ThreadPoolExecutor
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle_lexical.py", "tests/test_oracle_semantic.py",
         "tests/test_oracle_tree.py", "tests/test_oracle_verify.py", "tests/test_oracle_accept.py",
-        "tests/test_oracle_embedding.py", "tests/test_oracle_tree_paper.py"]
+        "tests/test_oracle_embedding.py", "tests/test_oracle_tree_paper.py", "tests/test_oracle_step.py"]
 
 MUTANTS = [
     ("js = np.arange(n - 1, L - 1)", "js = np.arange(n - 1, L)"),              # anchor counts itself
@@ -48,7 +48,21 @@ MUTANTS = [
     ("                token.append(int(M[best + 1]))", "                token.append(int(M[best]))"),   # the branch token again
     ("                s_b = cosine_rows(bank, [t - 1 for t in C], bank[j])", "                s_b = cosine_rows(bank, C, bank[j])"),
     ("            if b < 0 or b in branches or b == first:", "            if b < 0 or b in branches:"),  # main token kept as a branch
-    ("            C = [t for t in range(1, L - 1) if int(M[t]) == b]", "            C = [t for t in range(0, L - 1) if int(M[t]) == b]"),
+    ("    ts = list(range(1, L - 1))", "    ts = list(range(0, L - 1))"),          # an occurrence with no preceding state
+    ("        drafts_successors = succ_mode == SUCC_EVERY_BRANCH or kind == KIND_SEM",
+     "        drafts_successors = True"),                                          # Algorithm 1's strict branch ignored
+    ("        drafts_successors = succ_mode == SUCC_EVERY_BRANCH or kind == KIND_SEM",
+     "        drafts_successors = succ_mode == SUCC_EVERY_BRANCH or kind == KIND_LEX"),  # the two branches swapped
+    ("    if C or emb is None or not ts:\n        return C\n", "    return C\n"),       # no successor backoff
+    ("    if C or emb is None or not ts:\n", "    if emb is None or not ts:\n"),        # semantic set despite occurrences
+    ("    return [t for i, t in enumerate(ts) if s[i] >= tau]", "    return [t for i, t in enumerate(ts) if s[i] > tau]"),
+    ("    s = cosine_rows(E, np.arange(len(ts)), row(b))", "    s = cosine_rows(E, np.arange(len(ts)), row(int(M[L - 1])))"),
+    ("            Vc = bf16_bits_to_f64(vc_bits[b, :, :L])", "            Vc = bf16_bits_to_f64(kc_bits[b, :, :L])"),   # values read from the keys
+    ("            sc_ = (1.0 / np.sqrt(Q.shape[-1])) if scale is None else scale",
+     "            sc_ = (1.0 / Q.shape[-1]) if scale is None else scale"),
+    ("        qv = None if query_bits is None else bf16_bits_to_f64(query_bits[b])", "        qv = None"),
+    ("        kind, pos, sc = semantic_topk(H, qv, C, k, tau)", "        kind, pos, sc = semantic_topk(H, qv, C, k, None)"),
+    ("    seqs = range(B) if seqs is None else seqs", "    seqs = range(B)"),
     ("        main = list(range(j + 1, j + 1 + min(S + 1, L - 1 - j))) if kind == KIND_LEX else []",
      "        main = list(range(j + 1, j + 1 + min(S, L - 1 - j))) if kind == KIND_LEX else []"),
 ]
