@@ -63,6 +63,18 @@ def log(msg):
 
 
 MFMA_PEAK_BF16_TFLOPS = 2500.0
+WARM_SECONDS = 1.0      # stepping before the timed steps, so that clocks have settled
+SPREAD_BLOCKS = 9       # further blocks of K steps timed after the headline block
+
+
+def hit_rates(kinds):
+    """The retrieval-outcome rates of the paper's hit-rate analysis (Appendix
+    E.1): lexical hit, semantic hit, no hit, and the fallback's recovery rate
+    among lexical misses (None without a miss)."""
+    n_lex, n_sem, n_none = (int((kinds == k).sum()) for k in (1, 2, 0))
+    N = n_lex + n_sem + n_none
+    return {"R_lex": n_lex / N, "R_sem": n_sem / N, "R_none": n_none / N,
+            "R_rec": n_sem / (n_sem + n_none) if n_sem + n_none else None, "N": N}
 
 
 def algorithmic_work(cfg, lens, cand_count, node_count, node_depth):
@@ -291,6 +303,7 @@ def measure_embed(adapld, cfg, bufs, s, tokens, lens, x, steps, stream):
     return {"call": "adapld_semantic_topk_embed", "us": us_embed, "hidden_state_fallback_us": us_hidden,
             "algorithmic_bytes": byts, "tau": tau, "vocab": V,
             "kinds": {"lex": int((kind == 1).sum()), "sem": int((kind == 2).sum()), "none": int((kind == 0).sum())},
+            "hit_rates": hit_rates(kind),
             "note": "the paper's token-embedding fallback in place of the hidden-state one, back-to-back calls; "
                     "not part of the step"}
 
@@ -325,39 +338,42 @@ def measure_paper_tree(adapld, cfg, bufs, s, tokens, lens, x, steps, stream):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n * 1e3, out
 
-    def paper():
+    def paper(mode=adapld.SUCC_SEMANTIC_ONLY):
         return adapld.build_draft_tree_paper(tokens, lens, s["bank"], bufs.topk_pos, bufs.topk_count, bufs.kind,
-                                             top, cfg.S, T_max)
+                                             top, cfg.S, T_max, succ_mode=mode)
 
     def plain():
         return adapld.build_draft_tree(tokens, lens, bufs.topk_pos, bufs.topk_count, bufs.kind, cfg.W, cfg.S,
                                        cfg.T_max)
 
     us_plain, _ = timed(plain)
+    us_every, _ = timed(lambda: paper(adapld.SUCC_EVERY_BRANCH))
     us_paper, out = timed(paper)
     T = out[4].cpu().numpy()
-    # algorithmic bytes: every sequence's context scanned once for the branch
-    # tokens, one bank row per occurrence plus the anchor's, the table row,
-    # the outputs (four int32 arrays and the mask rows)
+    # algorithmic bytes (Algorithm 1's reading: successors after a semantic
+    # anchor only): a drafting sequence's context scanned once for its branch
+    # tokens and one bank row per occurrence, every anchor's row, the table
+    # row, the outputs (four int32 arrays and the mask rows)
     tok = x["tokens"]
     pos = bufs.topk_pos[:, 0].cpu().numpy()
     cnt = bufs.topk_count.cpu().numpy()
     kd = bufs.kind.cpu().numpy()
     topn = top.cpu().numpy()
     occ = 0
+    scanned = 0
     for b in range(B):
         L = int(min(max(x["lens"][b], 0), Ls))
         j = int(pos[b])
-        if cnt[b] < 1 or kd[b] == 0 or not 0 <= j <= L - 2:
+        if cnt[b] < 1 or kd[b] != 2 or not 0 <= j <= L - 2:
             continue
-        br = [t for t in dict.fromkeys(int(v) for v in topn[b, j])
-              if t >= 0 and not (kd[b] == 1 and t == tok[b, j + 1])]
+        br = [t for t in dict.fromkeys(int(v) for v in topn[b, j][:W]) if t >= 0]
         occ += int(np.isin(tok[b, 1:max(L - 1, 1)], br).sum())
+        scanned += L
     nw = (T_max + 63) // 64
-    byts = int(4 * int(np.clip(x["lens"], 0, Ls).sum()) + 2 * cfg.d * (occ + B) + 4 * W * B
-               + B * T_max * (16 + 8 * nw) + 4 * B)
+    byts = int(4 * scanned + 2 * cfg.d * (occ + B) + 4 * W * B + B * T_max * (16 + 8 * nw) + 4 * B)
     del top
-    return {"call": "adapld_build_draft_tree_paper", "us": us_paper, "ranked_list_tree_us": us_plain,
+    return {"call": "adapld_build_draft_tree_paper", "succ_mode": "semantic_only (Algorithm 1)", "us": us_paper,
+            "every_branch_us": us_every, "ranked_list_tree_us": us_plain,
             "algorithmic_bytes": byts, "achieved_GBs": byts / (us_paper * 1e-6) / 1e9, "occurrence_rows": occ, "nodes_mean": float(T.mean()), "T_max": T_max,
             "note": "the paper's construction (branch tokens from a synthetic top-W table, reranked successors) "
                     "in place of the ranked-list tree; back-to-back calls; not part of the step"}
@@ -420,16 +436,32 @@ def measure(adapld, cfg, name, make_inputs, args):
                              buffers=bufs, stream=stream) for j in range(n_copies)]
     for i in range(warmup):
         calls[i % n_copies]()
-    log(f"[bench] timing {steps} steps")
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
+    # Clocks settle only after some time under load: keep stepping until at
+    # least WARM_SECONDS of steps have run (on top of the W warm-up steps).
     torch.cuda.synchronize()
-    t_start.record(stream)
-    for i in range(steps):
-        calls[i % n_copies]()
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    step_ms = t_start.elapsed_time(t_end) / steps
+    t_warm = time.perf_counter()
+    n_warm = 0
+    while time.perf_counter() - t_warm < WARM_SECONDS:
+        for i in range(16):
+            calls[i % n_copies]()
+        n_warm += 16
+        torch.cuda.synchronize()
+    log(f"[bench] timing {steps} steps (after {warmup} + {n_warm} warm-up steps)")
+
+    def timed_block():
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for i in range(steps):
+            calls[i % n_copies]()
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        return t_start.elapsed_time(t_end) / steps
+
+    step_ms = timed_block()
+    # The spread of the same measurement: more blocks of K steps after it.
+    block_us = [timed_block() * 1e3 for _ in range(SPREAD_BLOCKS)]
     del calls
 
     # Instrumented timing: the same K steps as four calls with events before
@@ -498,6 +530,9 @@ def measure(adapld, cfg, name, make_inputs, args):
         "warmup": warmup,
         "ms_per_step": step_ms,
         "step_us": step_ms * 1e3,
+        "step_us_blocks_p10_p50_p90": [float(np.percentile(block_us, q)) for q in (10, 50, 90)],
+        "spread_blocks": SPREAD_BLOCKS,
+        "warm_up": {"steps": warmup, "steady_clock_steps": n_warm, "seconds": WARM_SECONDS},
         "instrumented_step_us_p10_p50_p90": [float(np.percentile(per_step_us, q)) for q in (10, 50, 90)],
         "higher_is_better": True,
         "scaling": "weak",
@@ -516,6 +551,7 @@ def measure(adapld, cfg, name, make_inputs, args):
         "draft_nodes_per_s": float(node_count.sum()) / (step_ms * 1e-3),
         "fallback_sequences": n_fb,
         "kinds": {"lex": int((kinds == 1).sum()), "sem": int((kinds == 2).sum()), "none": int((kinds == 0).sum())},
+        "hit_rates": hit_rates(kinds),
         "roofline": {"kernel": "tree_verify_attn", "bound": "hbm", "achieved": ver_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": ver_gbs / HBM_PEAK_GBS, "traffic": verify_traffic(name),
                      "algorithmic_bytes_per_launch": ver_b, "launch_us": ver_ms * 1e3},

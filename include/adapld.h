@@ -247,6 +247,11 @@ int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank
                 int32_t* node_depth, int32_t* node_src, int32_t* node_count, uint64_t* tree_mask,
                 uint16_t* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Which branch tokens of adapld_build_draft_tree_paper get a successor. */
+#define ADAPLD_SUCC_EVERY_BRANCH 0    /* every branch token (the text of Sec. 3.5) */
+#define ADAPLD_SUCC_SEMANTIC_ONLY 1   /* only after a semantic anchor (Algorithm 1: the
+                                         strict, lexical branch drafts no successor) */
+
 /*
  * adapld_build_draft_tree_paper -- the paper's own draft construction
  * (Sec. 3.5, Eqs. (8)-(15), Algorithm 1); an alternative to call 3 with the
@@ -259,11 +264,18 @@ int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank
  *   - the branch tokens: the entries of top_tokens[b, j*, 0..W-1] that are
  *     >= 0, not a repeat of an earlier entry and (on a lexical hit) not
  *     M[j*+1], in table order; each is a depth-0 node with src = -1;
- *   - right after each branch token c, its successor: among the occurrences
- *     t in [1, L-2] with M[t] == c, the one whose preceding hidden state
- *     bank[b, t-1] has the highest cosine with bank[b, j*] (ties: lowest t;
- *     fp32 scores as in adapld_semantic_topk); the node is M[t+1] at depth 1
- *     with src = t+1.  A branch token with no occurrence has no successor.
+ *   - right after each branch token c that drafts a successor (every one
+ *     under ADAPLD_SUCC_EVERY_BRANCH; under ADAPLD_SUCC_SEMANTIC_ONLY only
+ *     when kind is SEM), its successor.  The candidates are the occurrences
+ *     t in [1, L-2] with M[t] == c; when there is none and `emb` is given,
+ *     they are the positions t in [1, L-2] whose token embedding has cosine
+ *     >= tau with c's (the lexical-first backoff of Sec. 3.3 applied to the
+ *     successor query, as Sec. 3.5 states; a token id outside [0, V) has a
+ *     zero embedding, cosine 0).  The chosen t is the candidate whose
+ *     preceding hidden state bank[b, t-1] has the highest cosine with
+ *     bank[b, j*] (ties: lowest t; fp32 scores as in adapld_semantic_topk);
+ *     the node is M[t+1] at depth 1 with src = t+1.  A branch token without
+ *     candidates has no successor.
  * Node arrays and tree_mask have the layouts of adapld_build_draft_tree;
  * T <= (S+1) + 2W.  Entries at or beyond T are unspecified except the mask
  * rows, which are 0.
@@ -274,12 +286,18 @@ int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank
  *   top_tokens int32 [B, L_stride, W]  the target's top-W tokens predicted
  *                     after each position, best first; -1 marks an empty slot
  *   W                 1..64 branch tokens;  S >= 0 main-path copy length
+ *   succ_mode         ADAPLD_SUCC_EVERY_BRANCH or ADAPLD_SUCC_SEMANTIC_ONLY
+ *   emb               bf16 [V, d] token embeddings (same d as the bank,
+ *                     16-byte aligned) for the successor backoff, or NULL
+ *                     for lexical-only successor retrieval (V, tau ignored)
+ *   V, tau            rows of emb; the embedding threshold (finite)
  *   ws                workspace of adapld_workspace_bytes(
  *                     ADAPLD_OP_BUILD_DRAFT_TREE_PAPER, B, L_stride, d, W, ...)
  *                     (the k slot carries W), 16-byte aligned
  *
- * Errors: NULL_ARG; INVALID_ARG for bad sizes, T_max < (S+1) + 2W or
- * misaligned bank/ws; UNSUPPORTED for k > ADAPLD_MAX_K, W > 64,
+ * Errors: NULL_ARG; INVALID_ARG for bad sizes, T_max < (S+1) + 2W, a
+ * succ_mode other than the two above, V < 1 or tau not finite with emb, or
+ * misaligned bank/emb/ws; UNSUPPORTED for k > ADAPLD_MAX_K, W > 64,
  * d > ADAPLD_MAX_HIDDEN, T_max > ADAPLD_MAX_TREE_NODES,
  * B*W > ADAPLD_MAX_SEMANTIC_BATCH or B*W*L_stride > INT32_MAX;
  * WORKSPACE_TOO_SMALL.
@@ -287,7 +305,8 @@ int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank
 int adapld_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, const uint16_t* bank,
                                   int d, const int32_t* topk_pos, const int32_t* topk_count,
                                   const int32_t* kind, int k, const int32_t* top_tokens, int W,
-                                  int S, int B, int L_stride, int T_max, int32_t* node_token,
+                                  int S, int succ_mode, const uint16_t* emb, int V, float tau,
+                                  int B, int L_stride, int T_max, int32_t* node_token,
                                   int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
                                   int32_t* node_count, uint64_t* tree_mask, void* ws,
                                   size_t ws_bytes, hipStream_t stream);

@@ -21,6 +21,7 @@ OP_LEXICAL_MATCH, OP_SEMANTIC_TOPK, OP_BUILD_DRAFT_TREE, OP_TREE_VERIFY_ATTN = 1
 OP_SEMANTIC_TOPK_EMBED = 5
 OP_BUILD_DRAFT_TREE_PAPER = 6
 OP_STEP = 7
+SUCC_EVERY_BRANCH, SUCC_SEMANTIC_ONLY = 0, 1
 HEAD_DIM = 128
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadapld.so")
@@ -61,7 +62,8 @@ SIGNATURES = {
     "adapld_step": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 11 + [ctypes.c_float] * 2
                     + [ctypes.c_void_p] * 16 + [ctypes.c_size_t, ctypes.c_void_p]),
     "adapld_build_draft_tree_paper": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int] + [ctypes.c_void_p] * 3
-                                      + [ctypes.c_int] + [ctypes.c_void_p] + [ctypes.c_int] * 5
+                                      + [ctypes.c_int] + [ctypes.c_void_p] + [ctypes.c_int] * 3
+                                      + [ctypes.c_void_p, ctypes.c_int, ctypes.c_float] + [ctypes.c_int] * 3
                                       + [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p]),
     "adapld_tree_verify_attn": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -235,11 +237,14 @@ def build_draft_tree(tokens, lens, topk_pos, topk_count, kind, W, S, T_max=None,
 
 
 def build_draft_tree_paper(tokens, lens, bank, topk_pos, topk_count, kind, top_tokens, S, T_max=None, *,
+                           succ_mode=SUCC_EVERY_BRANCH, emb=None, tau=None,
                            node_token=None, node_parent=None, node_depth=None, node_src=None, node_count=None,
                            tree_mask=None, ws=None, stream=None):
     """The paper's draft tree (main path, branch tokens from the target's top
     tokens, reranked successors); returns (token, parent, depth, src, count,
-    mask).  top_tokens is int32 [B, L_stride, W]."""
+    mask).  top_tokens is int32 [B, L_stride, W]; succ_mode is
+    SUCC_EVERY_BRANCH or SUCC_SEMANTIC_ONLY; emb (bf16 [V, d]) and tau turn on
+    the successor retrieval's embedding backoff."""
     lib = load_library()
     B, L_stride, d = bank.shape
     k = topk_pos.shape[1]
@@ -255,11 +260,17 @@ def build_draft_tree_paper(tokens, lens, bank, topk_pos, topk_count, kind, top_t
     if ws is None:
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
     i32 = (torch.int32,)
+    if emb is not None:
+        if tau is None:
+            raise ValueError("the successor backoff needs tau")
+        if emb.dim() != 2 or emb.shape[1] != d:
+            raise ValueError(f"emb must be [V, {d}], got {tuple(emb.shape)}")
     st = lib.adapld_build_draft_tree_paper(
         _ptr(tokens, "tokens", i32, (B, L_stride)), _ptr(lens, "lens", i32, (B,)), _ptr(bank, "bank", _BF16_DTYPES),
         d, _ptr(topk_pos, "topk_pos", i32, (B, k)), _ptr(topk_count, "topk_count", i32, (B,)),
-        _ptr(kind, "kind", i32, (B,)), k, _ptr(top_tokens, "top_tokens", i32, (B, L_stride, W)), W, S, B,
-        L_stride, T_max,
+        _ptr(kind, "kind", i32, (B,)), k, _ptr(top_tokens, "top_tokens", i32, (B, L_stride, W)), W, S,
+        int(succ_mode), _ptr(emb, "emb", _BF16_DTYPES, nullable=True), 0 if emb is None else emb.shape[0],
+        float("nan") if tau is None else float(tau), B, L_stride, T_max,
         _ptr(node_token, "node_token", i32, (B, T_max)), _ptr(node_parent, "node_parent", i32, (B, T_max)),
         _ptr(node_depth, "node_depth", i32, (B, T_max)), _ptr(node_src, "node_src", i32, (B, T_max)),
         _ptr(node_count, "node_count", i32, (B,)),

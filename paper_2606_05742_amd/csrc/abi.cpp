@@ -9,7 +9,7 @@ namespace {
 
 thread_local int g_last_hip_error = 0;
 
-constexpr int kVersion = 10100;  // 1.1.0: adapld_step, adapld_build_draft_tree_paper
+constexpr int kVersion = 10200;  // 1.2.0: successor modes and backoff in adapld_build_draft_tree_paper
 
 bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
@@ -238,7 +238,8 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
 int adapld_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, const uint16_t* bank,
                                   int d, const int32_t* topk_pos, const int32_t* topk_count,
                                   const int32_t* kind, int k, const int32_t* top_tokens, int W,
-                                  int S, int B, int L_stride, int T_max, int32_t* node_token,
+                                  int S, int succ_mode, const uint16_t* emb, int V, float tau,
+                                  int B, int L_stride, int T_max, int32_t* node_token,
                                   int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
                                   int32_t* node_count, uint64_t* tree_mask, void* ws,
                                   size_t ws_bytes, hipStream_t stream) {
@@ -253,11 +254,14 @@ int adapld_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, co
       (int64_t)B * W > ADAPLD_MAX_SEMANTIC_BATCH || (int64_t)B * W * L_stride > INT32_MAX)
     return ADAPLD_ERR_UNSUPPORTED;
   if ((int64_t)S + 1 + 2LL * W > T_max) return ADAPLD_ERR_INVALID_ARG;
+  if (succ_mode != ADAPLD_SUCC_EVERY_BRANCH && succ_mode != ADAPLD_SUCC_SEMANTIC_ONLY)
+    return ADAPLD_ERR_INVALID_ARG;
+  if (emb && (V < 1 || !std::isfinite(tau) || misaligned16(emb))) return ADAPLD_ERR_INVALID_ARG;
   if (misaligned16(bank) || misaligned16(ws)) return ADAPLD_ERR_INVALID_ARG;
   if (ws_bytes < adapld::paper_tree_ws_bytes(B, L_stride, W, d)) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
   return hip_status(adapld::launch_build_draft_tree_paper(
-      tokens, lens, bank, d, topk_pos, topk_count, kind, k, top_tokens, W, S, B, L_stride, T_max,
-      node_token, node_parent, node_depth, node_src, node_count, tree_mask, ws, stream));
+      tokens, lens, bank, d, topk_pos, topk_count, kind, k, top_tokens, W, S, succ_mode, emb, V, tau, B,
+      L_stride, T_max, node_token, node_parent, node_depth, node_src, node_count, tree_mask, ws, stream));
 }
 
 int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx,

@@ -87,6 +87,7 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
                                    void* ws, const VerifyPlan& plan, hipStream_t stream);
 
 size_t embed_ws_bytes(int B, int L_stride);
+size_t embed_flag_bytes(int lists, int L_stride);
 
 // The paper's draft construction: branch tokens from the target's top tokens
 // after the anchor, each followed by its hidden-state-reranked successor.
@@ -95,7 +96,8 @@ size_t embed_ws_bytes(int B, int L_stride);
 size_t paper_tree_ws_bytes(int B, int L_stride, int W, int d);
 hipError_t launch_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, const uint16_t* bank, int d,
                                          const int32_t* topk_pos, const int32_t* topk_count, const int32_t* kind,
-                                         int k, const int32_t* top_tokens, int W, int S, int B, int L_stride,
+                                         int k, const int32_t* top_tokens, int W, int S, int succ_mode,
+                                         const uint16_t* emb, int V_emb, float tau, int B, int L_stride,
                                          int T_max, int32_t* node_token, int32_t* node_parent, int32_t* node_depth,
                                          int32_t* node_src, int32_t* node_count, uint64_t* tree_mask, void* ws,
                                          hipStream_t stream);
@@ -106,6 +108,15 @@ hipError_t launch_embedding_fallback(const int32_t* tokens, const int32_t* lens,
                                      const int32_t* cand_count, const uint16_t* emb, int V, int B,
                                      int L_stride, int d, float tau, void* ws, int32_t** cands,
                                      int32_t** counts, int32_t** kinds, hipStream_t stream);
+
+// The successor backoff of the paper's construction: for every list v (branch
+// v % W of sequence v / W) with skip[v] == 0, the positions t in [1, L-2] whose
+// token embedding has cosine >= tau with branch_tok[v]'s, written as rows
+// t - 1 in ascending order to lists[v] with their count.
+hipError_t launch_successor_embed(const int32_t* tokens, const int32_t* lens, const uint16_t* emb, int V,
+                                  int B, int W, int L_stride, int d, float tau, const int32_t* skip,
+                                  const int32_t* branch_tok, uint8_t* flags, int32_t* lists,
+                                  int32_t* counts, hipStream_t stream);
 
 hipError_t launch_accept_greedy(const int32_t* node_token, const int32_t* node_parent,
                                 const int32_t* node_depth, const int32_t* node_count,

@@ -18,6 +18,12 @@
 // the run counts (as the lexical kernel orders its hits).
 //
 // The rerank is the hidden-state scan and merge kernels in rerank-only mode.
+//
+// The same two kernels serve the successor retrieval of the paper's draft
+// construction (Sec. 3.5): there a "list" is one branch token of one
+// sequence, its query is the branch token's embedding, its positions are the
+// occurrence candidates t in [1, L-2] (flag index t - 1, the rerank row of
+// t), and a list is only scanned when the branch token never occurs.
 #include <cmath>
 
 #include "adapld_internal.h"
@@ -36,35 +42,39 @@ constexpr int kCompactPiece = kCompactThreads * kCompactRun;
 struct EmbedArgs {
   const int32_t* tokens;
   const int32_t* lens;
-  const int32_t* cand_pos;
-  const int32_t* cand_count;
+  const int32_t* cand_pos;   // lexical lists, copied through a skipped list (NULL: leave it)
+  const int32_t* skip;       // [lists] nonzero: the list takes no embedding set
+  const int32_t* qtok;       // [lists] query token (NULL: the sequence's last token)
   const uint16_t* emb;
   int V, B, L_stride, d, flag_stride;
+  int seq_div;               // list v belongs to sequence v / seq_div
+  int pos_off;               // flag i stands for position i + pos_off
   float tau;
-  uint8_t* flags;       // [B][flag_stride]
-  int32_t* out_pos;     // [B][L_stride]
-  int32_t* out_count;   // [B]
-  int32_t* out_kind;    // [B]
+  uint8_t* flags;       // [lists][flag_stride]
+  int32_t* out_pos;     // [lists][L_stride]
+  int32_t* out_count;   // [lists]
+  int32_t* out_kind;    // [lists] or NULL
 };
 
 // cos(emb[t], anchor) >= tau for one gathered row; a token outside [0, V) has
 // a zero embedding (cosine 0).
 template <int NIT>
 __global__ __launch_bounds__(kFlagWaves * kWave) void embed_flags_kernel(const EmbedArgs a) {
-  const int b = blockIdx.y;
+  const int v = blockIdx.y;
+  const int b = v / a.seq_div;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  if (a.cand_count[b] > 0) return;   // a lexical hit needs no flags
+  if (a.skip[v] != 0) return;        // e.g. a lexical hit needs no flags
   const int L = min(max(a.lens[b], 0), a.L_stride);
-  const int J = L - 1;               // positions [0, J)
+  const int J = L - 1 - a.pos_off;   // flags [0, J): positions [pos_off, L - 1)
   const int j0 = blockIdx.x * kPosPerWg + wave * kPosPerWave;
   if (j0 >= J) return;
   const int32_t* __restrict__ M = a.tokens + (size_t)b * a.L_stride;
   const int d = a.d;
 
-  const int at = M[L - 1];
+  const int at = a.qtok ? a.qtok[v] : M[L - 1];
   const bool a_ok = at >= 0 && at < a.V;
-  const int my_tok = lane < kPosPerWave && j0 + lane < J ? M[j0 + lane] : -1;
+  const int my_tok = lane < kPosPerWave && j0 + lane < J ? M[j0 + lane + a.pos_off] : -1;
   uint4 qv[NIT];
   float qn = 0.f;
 #pragma unroll
@@ -95,7 +105,7 @@ __global__ __launch_bounds__(kFlagWaves * kWave) void embed_flags_kernel(const E
       rv[it] = ok && e < d ? *reinterpret_cast<const uint4*>(a.emb + (size_t)t * d + e) : make_uint4(0, 0, 0, 0);
     }
   };
-  uint8_t* __restrict__ fl = a.flags + (size_t)b * a.flag_stride;
+  uint8_t* __restrict__ fl = a.flags + (size_t)v * a.flag_stride;
   const int n = min(kPosPerWave, J - j0);
   for (int i = 0; i < n; i += 2) {
     uint4 r0[NIT], r1[NIT];
@@ -114,24 +124,27 @@ __global__ __launch_bounds__(kFlagWaves * kWave) void embed_flags_kernel(const E
 
 __global__ __launch_bounds__(kCompactThreads) void embed_compact_kernel(const EmbedArgs a) {
   __shared__ int s_red[kCompactThreads / kWave];
-  const int b = blockIdx.x;
+  const int v = blockIdx.x;
+  const int b = v / a.seq_div;
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid / kWave;
-  const int cc = min(max(a.cand_count[b], 0), a.L_stride);
-  int32_t* __restrict__ out = a.out_pos + (size_t)b * a.L_stride;
-  if (cc > 0) {   // the backoff rule: a lexical set is the result
-    const int32_t* __restrict__ in = a.cand_pos + (size_t)b * a.L_stride;
-    for (int i = tid; i < cc; i += kCompactThreads) out[i] = in[i];
-    if (tid == 0) {
-      a.out_count[b] = cc;
-      a.out_kind[b] = ADAPLD_KIND_LEX;
+  int32_t* __restrict__ out = a.out_pos + (size_t)v * a.L_stride;
+  if (a.skip[v] != 0) {
+    if (a.cand_pos) {   // the backoff rule: a lexical set is the result
+      const int cc = min(max(a.skip[v], 0), a.L_stride);
+      const int32_t* __restrict__ in = a.cand_pos + (size_t)v * a.L_stride;
+      for (int i = tid; i < cc; i += kCompactThreads) out[i] = in[i];
+      if (tid == 0) {
+        a.out_count[v] = cc;
+        if (a.out_kind) a.out_kind[v] = ADAPLD_KIND_LEX;
+      }
     }
     return;
   }
   const int L = min(max(a.lens[b], 0), a.L_stride);
-  const int J = max(L - 1, 0);
-  const uint8_t* __restrict__ fl = a.flags + (size_t)b * a.flag_stride;
+  const int J = max(L - 1 - a.pos_off, 0);
+  const uint8_t* __restrict__ fl = a.flags + (size_t)v * a.flag_stride;
   int total = 0;
   for (int p0 = 0; p0 < J; p0 += kCompactPiece) {
     // Thread tid owns positions [q0, q0 + 32) of this piece (16-byte aligned).
@@ -166,8 +179,8 @@ __global__ __launch_bounds__(kCompactThreads) void embed_compact_kernel(const Em
     total += piece;
   }
   if (tid == 0) {
-    a.out_count[b] = total;
-    a.out_kind[b] = total > 0 ? ADAPLD_KIND_SEM : ADAPLD_KIND_NONE;
+    a.out_count[v] = total;
+    if (a.out_kind) a.out_kind[v] = total > 0 ? ADAPLD_KIND_SEM : ADAPLD_KIND_NONE;
   }
 }
 
@@ -177,36 +190,18 @@ void launch_flags(const EmbedArgs& a, int B, hipStream_t stream) {
   hipLaunchKernelGGL(embed_flags_kernel<NIT>, grid, dim3(kFlagWaves * kWave), 0, stream, a);
 }
 
-}  // namespace
-
-size_t embed_ws_bytes(int B, int L_stride) {
-  // flags (rows padded to whole 32-flag runs of the compaction, 16-byte
-  // aligned), then the candidate list, its size and its kind
-  const size_t stride = ((size_t)L_stride + kCompactRun - 1) / kCompactRun * kCompactRun;
-  return (size_t)B * stride + (size_t)B * L_stride * 4 + (size_t)B * 8;
+size_t flag_stride_of(int L_stride) {
+  return ((size_t)L_stride + kCompactRun - 1) / kCompactRun * kCompactRun;
 }
 
-hipError_t launch_embedding_fallback(const int32_t* tokens, const int32_t* lens, const int32_t* cand_pos,
-                                     const int32_t* cand_count, const uint16_t* emb, int V, int B,
-                                     int L_stride, int d, float tau, void* ws, int32_t** cands,
-                                     int32_t** counts, int32_t** kinds, hipStream_t stream) {
-  const size_t stride = ((size_t)L_stride + kCompactRun - 1) / kCompactRun * kCompactRun;
-  uint8_t* base = static_cast<uint8_t*>(ws);
-  EmbedArgs a{};
-  a.tokens = tokens; a.lens = lens; a.cand_pos = cand_pos; a.cand_count = cand_count; a.emb = emb;
-  a.V = V; a.B = B; a.L_stride = L_stride; a.d = d; a.flag_stride = (int)stride; a.tau = tau;
-  a.flags = base;
-  a.out_pos = reinterpret_cast<int32_t*>(base + (size_t)B * stride);
-  a.out_count = a.out_pos + (size_t)B * L_stride;
-  a.out_kind = a.out_count + B;
-  *cands = a.out_pos;
-  *counts = a.out_count;
-  *kinds = a.out_kind;
-  const int nit = (d + 8 * kWave - 1) / (8 * kWave);
+// The flags kernel (one instantiation per 512-element slice count of d),
+// then the compaction.
+hipError_t launch_embed_lists(const EmbedArgs& a, int lists, hipStream_t stream) {
+  const int nit = (a.d + 8 * kWave - 1) / (8 * kWave);
   switch (nit) {
 #define ADAPLD_FLAGS_CASE(n) \
   case n:                    \
-    launch_flags<n>(a, B, stream); \
+    launch_flags<n>(a, lists, stream); \
     break;
     ADAPLD_FLAGS_CASE(1) ADAPLD_FLAGS_CASE(2) ADAPLD_FLAGS_CASE(3) ADAPLD_FLAGS_CASE(4)
     ADAPLD_FLAGS_CASE(5) ADAPLD_FLAGS_CASE(6) ADAPLD_FLAGS_CASE(7) ADAPLD_FLAGS_CASE(8)
@@ -218,8 +213,50 @@ hipError_t launch_embedding_fallback(const int32_t* tokens, const int32_t* lens,
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(embed_compact_kernel, dim3(B), dim3(kCompactThreads), 0, stream, a);
+  hipLaunchKernelGGL(embed_compact_kernel, dim3(lists), dim3(kCompactThreads), 0, stream, a);
   return hipGetLastError();
+}
+
+}  // namespace
+
+size_t embed_ws_bytes(int B, int L_stride) {
+  // flags (rows padded to whole 32-flag runs of the compaction, 16-byte
+  // aligned), then the candidate list, its size and its kind
+  return (size_t)B * flag_stride_of(L_stride) + (size_t)B * L_stride * 4 + (size_t)B * 8;
+}
+
+size_t embed_flag_bytes(int lists, int L_stride) { return (size_t)lists * flag_stride_of(L_stride); }
+
+hipError_t launch_embedding_fallback(const int32_t* tokens, const int32_t* lens, const int32_t* cand_pos,
+                                     const int32_t* cand_count, const uint16_t* emb, int V, int B,
+                                     int L_stride, int d, float tau, void* ws, int32_t** cands,
+                                     int32_t** counts, int32_t** kinds, hipStream_t stream) {
+  const size_t stride = flag_stride_of(L_stride);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  EmbedArgs a{};
+  a.tokens = tokens; a.lens = lens; a.cand_pos = cand_pos; a.skip = cand_count; a.qtok = nullptr;
+  a.emb = emb; a.V = V; a.B = B; a.L_stride = L_stride; a.d = d; a.flag_stride = (int)stride;
+  a.seq_div = 1; a.pos_off = 0; a.tau = tau;
+  a.flags = base;
+  a.out_pos = reinterpret_cast<int32_t*>(base + (size_t)B * stride);
+  a.out_count = a.out_pos + (size_t)B * L_stride;
+  a.out_kind = a.out_count + B;
+  *cands = a.out_pos;
+  *counts = a.out_count;
+  *kinds = a.out_kind;
+  return launch_embed_lists(a, B, stream);
+}
+
+hipError_t launch_successor_embed(const int32_t* tokens, const int32_t* lens, const uint16_t* emb, int V,
+                                  int B, int W, int L_stride, int d, float tau, const int32_t* skip,
+                                  const int32_t* branch_tok, uint8_t* flags, int32_t* lists,
+                                  int32_t* counts, hipStream_t stream) {
+  EmbedArgs a{};
+  a.tokens = tokens; a.lens = lens; a.cand_pos = nullptr; a.skip = skip; a.qtok = branch_tok;
+  a.emb = emb; a.V = V; a.B = B * W; a.L_stride = L_stride; a.d = d;
+  a.flag_stride = (int)flag_stride_of(L_stride); a.seq_div = W; a.pos_off = 1; a.tau = tau;
+  a.flags = flags; a.out_pos = lists; a.out_count = counts; a.out_kind = nullptr;
+  return launch_embed_lists(a, B * W, stream);
 }
 
 }  // namespace adapld

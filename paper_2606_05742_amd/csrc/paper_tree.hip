@@ -12,6 +12,16 @@
 // W lists of a sequence share one query, the anchor's hidden state H[j*],
 // copied once per sequence.
 //
+// successor backoff (with an embedding table): a branch token that never
+// occurs in [1, L-2] takes instead the positions whose token embedding is
+// within tau of its own (Sec. 3.5 applies the lexical-first backoff of
+// Sec. 3.3 to the successor query), from the embedding flag and compaction
+// kernels run over the B*W lists.
+//
+// Successors are drafted for every branch (the text of Sec. 3.5) or only
+// after a semantic anchor (Algorithm 1's strict branch drafts none),
+// selected by succ_mode.
+//
 // rerank: the hidden-state scan and merge with k = 1 over the B*W lists (a
 // list reads the bank rows and the query of its sequence), so the argmax of
 // cos(H[t-1], H[j*]) costs one pass over the candidate rows of all branches
@@ -37,6 +47,7 @@ struct PaperTreeArgs {
   const int32_t* kind;
   const int32_t* top_tokens;   // [B][L_stride][W]
   int k, W, S, B, L_stride, d, T_max;
+  int succ_mode;               // ADAPLD_SUCC_*
   // workspace
   int32_t* btok;     // [B][W] branch tokens
   int32_t* nbr;      // [B]    number of branches
@@ -48,6 +59,7 @@ struct PaperTreeArgs {
   float* vscore;
   int32_t* vcnt;     // [B*W]  1 if the branch has a successor
   int32_t* vkind;
+  int32_t* vskip;    // [B*W]  nonzero: no embedding backoff for the list
   // outputs
   int32_t* node_token;
   int32_t* node_parent;
@@ -144,10 +156,7 @@ __global__ __launch_bounds__(kSetupThreads) void paper_tree_setup_kernel(const P
     }
     const uint64_t keep = __ballot(ok);
     const int idx = __popcll(keep & lanes_below());
-    if (ok) {
-      s_tok[idx] = tok;
-      a.btok[(size_t)b * a.W + idx] = tok;
-    }
+    if (ok) s_tok[idx] = tok;
     if (lane < a.W) s_cnt[lane] = 0;
     if (lane == 0) {
       s_nb = __popcll(keep);
@@ -156,12 +165,15 @@ __global__ __launch_bounds__(kSetupThreads) void paper_tree_setup_kernel(const P
   }
   __syncthreads();
   const int nb = s_nb;
+  // Algorithm 1 drafts no successor after a lexical anchor.
+  const bool drafts = j >= 0 && (a.succ_mode == ADAPLD_SUCC_EVERY_BRANCH || kd == ADAPLD_KIND_SEM);
+  const int nscan = drafts ? nb : 0;
   // One pass over the context for all branch tokens: occurrence t (with a
   // preceding hidden state and a following token, t in [1, L-2]) of branch i
   // adds row t-1 to list i.  Per branch a thread compares its tokens in
   // registers into a 32-bit mask, takes that many slots and writes the rows.
   // List order is arbitrary: the rerank breaks ties by position.
-  for (int base = 0; nb > 0 && base < L; base += kSetupPass) {
+  for (int base = 0; nscan > 0 && base < L; base += kSetupPass) {
     if (base > 0) load_pass(base);
     uint32_t valid = 0;   // bit 4i+e: token e of load i is an occurrence position
 #pragma unroll
@@ -170,7 +182,7 @@ __global__ __launch_bounds__(kSetupThreads) void paper_tree_setup_kernel(const P
 #pragma unroll
       for (int e = 0; e < 4; ++e) valid |= (t0 + e >= 1 && t0 + e <= L - 2 ? 1u : 0u) << (4 * i + e);
     }
-    for (int br = 0; br < nb; ++br) {
+    for (int br = 0; br < nscan; ++br) {
       const int c = s_tok[br];
       uint32_t hit = 0;
 #pragma unroll
@@ -204,8 +216,11 @@ __global__ __launch_bounds__(kSetupThreads) void paper_tree_setup_kernel(const P
   __syncthreads();
   if (tid < a.W) {
     const size_t v = (size_t)b * a.W + tid;
-    a.vcount[v] = tid < nb ? s_cnt[tid] : 0;
+    const int cnt = tid < nscan ? s_cnt[tid] : 0;
+    a.vcount[v] = cnt;
     a.vlens[v] = L;
+    a.vskip[v] = tid < nscan && cnt == 0 ? 0 : 1;   // a drafted branch token with no occurrence
+    a.btok[v] = tid < nb ? s_tok[tid] : -1;
   }
 }
 
@@ -288,18 +303,21 @@ size_t paper_tree_ws_bytes(int B, int L_stride, int W, int d) {
   size_t n = 0;
   n += V * 4 + (size_t)B * 4;            // btok, nbr
   n += V * L_stride * 4;                 // vcand
-  n += V * 4 * 2;                        // vcount, vlens
+  n += V * 4 * 3;                        // vcount, vlens, vskip
   n = (n + 15) / 16 * 16;
   n += (size_t)B * d * 2;                // vquery
   n += V * 4 * 4;                        // vpos, vscore, vcnt, vkind
   n = (n + 15) / 16 * 16;
   n += V * scan_lists(L_stride) * 8;     // the rerank's lists (k = 1)
+  n = (n + 15) / 16 * 16;
+  n += embed_flag_bytes((int)V, L_stride);   // the successor backoff's flags
   return n;
 }
 
 hipError_t launch_build_draft_tree_paper(const int32_t* tokens, const int32_t* lens, const uint16_t* bank, int d,
                                          const int32_t* topk_pos, const int32_t* topk_count, const int32_t* kind,
-                                         int k, const int32_t* top_tokens, int W, int S, int B, int L_stride,
+                                         int k, const int32_t* top_tokens, int W, int S, int succ_mode,
+                                         const uint16_t* emb, int V_emb, float tau, int B, int L_stride,
                                          int T_max, int32_t* node_token, int32_t* node_parent, int32_t* node_depth,
                                          int32_t* node_src, int32_t* node_count, uint64_t* tree_mask, void* ws,
                                          hipStream_t stream) {
@@ -307,6 +325,7 @@ hipError_t launch_build_draft_tree_paper(const int32_t* tokens, const int32_t* l
   a.tokens = tokens; a.lens = lens; a.bank = bank; a.topk_pos = topk_pos; a.topk_count = topk_count;
   a.kind = kind; a.top_tokens = top_tokens;
   a.k = k; a.W = W; a.S = S; a.B = B; a.L_stride = L_stride; a.d = d; a.T_max = T_max;
+  a.succ_mode = succ_mode;
   const size_t V = (size_t)B * W;
   char* p = static_cast<char*>(ws);
   size_t off = 0;
@@ -315,6 +334,7 @@ hipError_t launch_build_draft_tree_paper(const int32_t* tokens, const int32_t* l
   a.vcand = reinterpret_cast<int32_t*>(p + off); off += V * L_stride * 4;
   a.vcount = reinterpret_cast<int32_t*>(p + off); off += V * 4;
   a.vlens = reinterpret_cast<int32_t*>(p + off); off += V * 4;
+  a.vskip = reinterpret_cast<int32_t*>(p + off); off += V * 4;
   off = (off + 15) / 16 * 16;
   a.vquery = reinterpret_cast<uint16_t*>(p + off); off += (size_t)B * d * 2;
   a.vpos = reinterpret_cast<int32_t*>(p + off); off += V * 4;
@@ -322,13 +342,20 @@ hipError_t launch_build_draft_tree_paper(const int32_t* tokens, const int32_t* l
   a.vcnt = reinterpret_cast<int32_t*>(p + off); off += V * 4;
   a.vkind = reinterpret_cast<int32_t*>(p + off); off += V * 4;
   off = (off + 15) / 16 * 16;
-  uint64_t* keys = reinterpret_cast<uint64_t*>(p + off);
+  uint64_t* keys = reinterpret_cast<uint64_t*>(p + off); off += V * scan_lists(L_stride) * 8;
+  off = (off + 15) / 16 * 16;
+  uint8_t* flags = reinterpret_cast<uint8_t*>(p + off);
   a.node_token = node_token; a.node_parent = node_parent; a.node_depth = node_depth; a.node_src = node_src;
   a.node_count = node_count; a.tree_mask = tree_mask;
 
   hipLaunchKernelGGL(paper_tree_setup_kernel, dim3(B), dim3(kSetupThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (emb) {
+    e = launch_successor_embed(tokens, lens, emb, V_emb, B, W, L_stride, d, tau, a.vskip, a.btok, flags, a.vcand,
+                               a.vcount, stream);
+    if (e != hipSuccess) return e;
+  }
   e = launch_semantic_topk(bank, a.vquery, a.vlens, a.vcand, a.vcount, (int)V, L_stride, d, 1, NAN, a.vpos,
                            a.vscore, a.vcnt, a.vkind, keys, nullptr, 1, stream, W);
   if (e != hipSuccess) return e;

@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(lib):
 def test_status_strings(lib):
     for code in (OK, NULL, INVALID, UNSUPPORTED, WS_SMALL, -5, 123):
         assert lib.adapld_status_string(code)
-    assert lib.adapld_version() == 10100
+    assert lib.adapld_version() == 10200
     assert lib.adapld_last_hip_error() == 0
 
 
@@ -133,7 +133,8 @@ def test_paper_tree_validation(lib):
     f = lib.adapld_build_draft_tree_paper
     args = lambda **kw: [kw.get(n, v) for n, v in (  # noqa: E731
         ("tokens", P), ("lens", P), ("bank", P), ("d", 128), ("pos", P), ("count", P), ("kind", P), ("k", 8),
-        ("top", P), ("W", 4), ("S", 12), ("B", 2), ("L_stride", 64), ("T_max", 21),
+        ("top", P), ("W", 4), ("S", 12), ("succ_mode", 0), ("emb", N), ("V", 0), ("tau", float("nan")),
+        ("B", 2), ("L_stride", 64), ("T_max", 21),
         ("nt", P), ("np", P), ("nd", P), ("ns", P), ("nc", P), ("mask", P), ("ws", P), ("ws_bytes", 1 << 30),
         ("stream", N))]
     assert f(*args(B=0)) == OK
@@ -151,6 +152,13 @@ def test_paper_tree_validation(lib):
     assert f(*args(B=513)) == UNSUPPORTED                 # B*W lists > 2048
     assert f(*args(bank=ctypes.c_void_p(0x10008))) == INVALID
     assert f(*args(ws=ctypes.c_void_p(0x10008))) == INVALID
+    assert f(*args(B=0, succ_mode=2)) == OK               # B = 0 returns before any check
+    assert f(*args(succ_mode=2)) == INVALID               # neither reading
+    assert f(*args(succ_mode=-1)) == INVALID
+    assert f(*args(emb=P, V=0, tau=0.5)) == INVALID        # an embedding table needs rows
+    assert f(*args(emb=P, V=10, tau=float("nan"))) == INVALID
+    assert f(*args(emb=P, V=10, tau=float("inf"))) == INVALID
+    assert f(*args(emb=ctypes.c_void_p(0x10008), V=10, tau=0.5)) == INVALID
     need = lib.adapld_workspace_bytes(6, 2, 64, 128, 4, 0, 0, 0, 0)
     assert need >= 2 * 4 * 64 * 4 + 2 * 4 * 128 * 2     # candidate lists + queries
     assert f(*args(ws_bytes=need - 1)) == WS_SMALL

@@ -36,9 +36,10 @@ def margin_ok(E, tokens, lens, tau, margin=1e-3):
     return True
 
 
-def run_and_check(cfg, x, E_bits, tau, k, ctx):
+def run_and_check(cfg, x, E_bits, tau, k, ctx, exact=False):
+    """exact: the table's cosines are exact in fp32 (no margin around tau needed)."""
     E = oracle.bf16_bits_to_f64(E_bits)
-    assert margin_ok(E, x["tokens"], x["lens"], tau), "pick another tau: a cosine sits on it"
+    assert exact or margin_ok(E, x["tokens"], x["lens"], tau), "pick another tau: a cosine sits on it"
     tokens, lens = dev_i32(x["tokens"]), dev_i32(x["lens"])
     cp, cc, mn = adapld.lexical_match(tokens, lens, cfg.n_max)
     pos, sc, cnt, kind = adapld.semantic_topk_embed(dev_bf16(x["bank"]), tokens, lens, cp, cc, dev_bf16(E_bits),
@@ -122,3 +123,27 @@ def test_embedding_fallback_out_of_range_tokens():
             assert int(kind[b]) == ekind, (tau, b)
             if ekind == oracle.KIND_SEM and len(Cs) <= 64:
                 assert sorted(int(p) for p in pos[b, :int(cnt[b])]) == sorted(Cs), (tau, b)
+
+
+@pytest.mark.parametrize("tau", [0.5, 0.25, 0.0, -0.5])
+def test_embedding_fallback_threshold_equality(tau):
+    """Eq. (4) keeps cos >= tau.  Embeddings of four +-1 entries among the
+    first 8 dimensions (norm 2) have cosines that are multiples of 1/4, exact
+    in fp32 and float64, so tau lands exactly on cosines present and the
+    kind and the candidate set must follow the >= rule bit for bit."""
+    cfg = small_config(B=8, L=600, d=128, k=64, n_max=3, seed=161, V=60, forced_every=1)
+    x = make_inputs(cfg, with_verify=False)
+    rng = np.random.default_rng(21)
+    V = cfg.V + 8
+    E = np.zeros((V, 128))
+    for r in range(V):
+        E[r, rng.choice(8, size=4, replace=False)] = rng.choice([-1.0, 1.0], size=4)
+    E_bits = f32_to_bf16_bits(E.astype(np.float32))
+    on = 0
+    for b in range(cfg.B):
+        L = int(x["lens"][b])
+        s = oracle.cosine_rows(E, x["tokens"][b, :L - 1], E[int(x["tokens"][b, L - 1])])
+        on += int(np.sum(s == tau))
+    assert on > 0, "no cosine sits exactly on tau"
+    kinds = run_and_check(cfg, x, E_bits, tau, 64, f"tau={tau} exact", exact=True)
+    assert oracle.KIND_SEM in kinds or oracle.KIND_NONE in kinds
