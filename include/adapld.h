@@ -253,6 +253,37 @@ int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank
                                          strict, lexical branch drafts no successor) */
 
 /*
+ * adapld_step_noalloc -- adapld_step for callers that cannot allocate device
+ * memory (code under HIP graph capture, serving loops or harnesses that
+ * forbid hipMalloc): the same arguments without `ws` and `ws_bytes`, the same
+ * validation, kernels and outputs.  The workspace is a device array inside
+ * the library, ADAPLD_NOALLOC_SCRATCH_BYTES per GPU, that each GPU holds
+ * from its first call until the process ends; the call itself allocates
+ * nothing.  The device current on the calling thread must be the one that
+ * `stream` and the buffers belong to.
+ *
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (other streams, other threads) race and give undefined
+ * results.  No part of the array has to start at zero.
+ *
+ * Errors: those of adapld_step; WORKSPACE_TOO_SMALL when
+ * adapld_workspace_bytes(ADAPLD_OP_STEP, ...) for these sizes exceeds
+ * ADAPLD_NOALLOC_SCRATCH_BYTES; HIP when the array's address cannot be
+ * looked up (see adapld_last_hip_error).
+ */
+#define ADAPLD_NOALLOC_SCRATCH_BYTES (64u << 20)
+int adapld_step_noalloc(const int32_t* tokens, const int32_t* lens, const uint16_t* bank,
+                        const uint16_t* query, const uint16_t* q, const uint16_t* k_ctx,
+                        const uint16_t* v_ctx, const uint16_t* k_tree, const uint16_t* v_tree, int B,
+                        int L_stride, int d, int n_max, int k, int W, int S, int T_max, int Hq,
+                        int Hkv, int D, float tau, float scale, int32_t* cand_pos,
+                        int32_t* cand_count, int32_t* match_n, int32_t* topk_pos, float* topk_score,
+                        int32_t* topk_count, int32_t* kind, int32_t* node_token,
+                        int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
+                        int32_t* node_count, uint64_t* tree_mask, uint16_t* out, float* lse,
+                        hipStream_t stream);
+
+/*
  * adapld_build_draft_tree_paper -- the paper's own draft construction
  * (Sec. 3.5, Eqs. (8)-(15), Algorithm 1); an alternative to call 3 with the
  * same outputs.

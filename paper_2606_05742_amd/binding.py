@@ -61,6 +61,8 @@ SIGNATURES = {
         ctypes.c_void_p, ctypes.c_void_p]),
     "adapld_step": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 11 + [ctypes.c_float] * 2
                     + [ctypes.c_void_p] * 16 + [ctypes.c_size_t, ctypes.c_void_p]),
+    "adapld_step_noalloc": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 11 + [ctypes.c_float] * 2
+                            + [ctypes.c_void_p] * 15 + [ctypes.c_void_p]),
     "adapld_build_draft_tree_paper": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int] + [ctypes.c_void_p] * 3
                                       + [ctypes.c_int] + [ctypes.c_void_p] + [ctypes.c_int] * 3
                                       + [ctypes.c_void_p, ctypes.c_int, ctypes.c_float] + [ctypes.c_int] * 3
@@ -396,7 +398,7 @@ class StepCall:
     The stream is the one given, else the current stream at construction."""
 
     def __init__(self, tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None,
-                 query=None, scale=None, buffers: StepBuffers | None = None, stream=None):
+                 query=None, scale=None, buffers: StepBuffers | None = None, stream=None, noalloc=False):
         B, L_stride = tokens.shape
         _, _, d = bank.shape
         _, T_max, Hq, D = q.shape
@@ -405,13 +407,14 @@ class StepCall:
             buffers = StepBuffers.allocate(B, L_stride, d, k, T_max, Hq, Hkv, D, device=tokens.device)
         bf = self.buffers = buffers
         need = workspace_bytes(OP_STEP, B, L_stride, d, k, T_max, Hq, Hkv, D)
-        if bf.ws_step.numel() < need:
+        if not noalloc and bf.ws_step.numel() < need:
             raise AdapldError(-4, f"buffers.ws_step holds {bf.ws_step.numel()} bytes, {need} needed")
         scale = 1.0 / math.sqrt(D) if scale is None else scale
         tau = float("nan") if tau is None else float(tau)
         i32, bf16 = (torch.int32,), _BF16_DTYPES
         nw = (T_max + 63) // 64
-        self._fn = load_library().adapld_step
+        self._name = "adapld_step_noalloc" if noalloc else "adapld_step"
+        self._fn = getattr(load_library(), self._name)
         self._args = (
             _ptr(tokens, "tokens", i32, (B, L_stride)), _ptr(lens, "lens", i32, (B,)),
             _ptr(bank, "bank", bf16), _ptr(query, "query", bf16, (B, d), nullable=True),
@@ -427,26 +430,30 @@ class StepCall:
             _ptr(bf.node_depth, "node_depth", i32, (B, T_max)), _ptr(bf.node_src, "node_src", i32, (B, T_max)),
             _ptr(bf.node_count, "node_count", i32, (B,)),
             _ptr(bf.tree_mask, "tree_mask", (torch.int64, torch.uint64), (B, T_max, nw)),
-            _ptr(bf.out, "out", bf16, (B, T_max, Hq, D)), _ptr(bf.lse, "lse", (torch.float32,), (B, Hq, T_max)),
-            _ptr(bf.ws_step, "ws_step", (torch.uint8,)), bf.ws_step.numel(), _stream(stream))
+            _ptr(bf.out, "out", bf16, (B, T_max, Hq, D)), _ptr(bf.lse, "lse", (torch.float32,), (B, Hq, T_max)))
+        # adapld_step_noalloc takes no workspace: its own device array serves
+        self._args += (() if noalloc else (_ptr(bf.ws_step, "ws_step", (torch.uint8,)), bf.ws_step.numel()))
+        self._args += (_stream(stream),)
         # keep every tensor alive as long as the call can be made
         self._keep = (tokens, lens, bank, query, q, k_ctx, v_ctx, k_tree, v_tree)
 
     def __call__(self) -> StepBuffers:
-        _check(self._fn(*self._args), "adapld_step")
+        _check(self._fn(*self._args), self._name)
         return self.buffers
 
 
 def step(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None, query=None,
-         scale=None, buffers: StepBuffers | None = None, stream=None):
+         scale=None, buffers: StepBuffers | None = None, stream=None, noalloc=False):
     """One draft-and-verify step: adapld_step, i.e. the four entry points
-    back to back on one stream from one native call.
+    back to back on one stream from one native call (adapld_step_noalloc
+    with noalloc=True: the library's own device workspace, nothing allocated
+    by the call).
 
     No host synchronisation happens inside; the lexical-hit / fallback decision
     is taken on the device.  Returns the StepBuffers holding every output.
     """
     return StepCall(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, n_max=n_max, k=k, W=W, S=S, tau=tau,
-                    query=query, scale=scale, buffers=buffers, stream=stream)()
+                    query=query, scale=scale, buffers=buffers, stream=stream, noalloc=noalloc)()
 
 
 def step_calls(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None, query=None,

@@ -9,7 +9,7 @@ namespace {
 
 thread_local int g_last_hip_error = 0;
 
-constexpr int kVersion = 10200;  // 1.2.0: successor modes and backoff in adapld_build_draft_tree_paper
+constexpr int kVersion = 10300;  // 1.3.0: adapld_step_noalloc
 
 bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
@@ -101,6 +101,11 @@ int check_verify(const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx
 }
 
 }  // namespace
+
+int adapld::record_hip_error(hipError_t e) {
+  g_last_hip_error = static_cast<int>(e);
+  return ADAPLD_ERR_HIP;
+}
 
 extern "C" {
 

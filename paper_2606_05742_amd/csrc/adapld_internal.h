@@ -45,6 +45,10 @@ struct VerifyPlan {
 VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv);
 size_t verify_ws_bytes(const VerifyPlan& p, int B, int Hkv);
 
+// Stores e as the calling thread's adapld_last_hip_error and returns
+// ADAPLD_ERR_HIP.
+int record_hip_error(hipError_t e);
+
 // ---------------------------------------------------------------- launchers
 // Each returns the hipError_t of its launches (hipSuccess on success).
 hipError_t launch_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride,

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     for n in names:
         assert hasattr(lib, n), n
         assert n in binding.SIGNATURES, n
@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(lib):
 def test_status_strings(lib):
     for code in (OK, NULL, INVALID, UNSUPPORTED, WS_SMALL, -5, 123):
         assert lib.adapld_status_string(code)
-    assert lib.adapld_version() == 10200
+    assert lib.adapld_version() == 10300
     assert lib.adapld_last_hip_error() == 0
 
 
@@ -251,3 +251,19 @@ def test_binding_refuses_cpu_tensors():
     t = torch.zeros((2, 8), dtype=torch.int32)
     with pytest.raises(binding.AdapldError):
         binding.lexical_match(t, torch.zeros(2, dtype=torch.int32), 2)
+
+
+def test_step_noalloc_validation(lib):
+    """The allocation-free step refuses, before any HIP call, sizes whose
+    workspace exceeds its device array (host-only checks: no GPU needed)."""
+    f = lib.adapld_step_noalloc
+    cap = 64 << 20
+    args = lambda **kw: [kw.get(n, v) for n, v in (  # noqa: E731
+        *((f"p{i}", P) for i in range(9)), ("B", 2), ("L_stride", 64), ("d", 128), ("n_max", 3), ("k", 8),
+        ("W", 4), ("S", 4), ("T_max", 20), ("Hq", 8), ("Hkv", 2), ("D", 128), ("tau", float("nan")), ("scale", 0.1),
+        *((f"o{i}", P) for i in range(15)), ("stream", N))]
+    assert f(*args(B=0)) == OK
+    assert f(*args(B=-1)) == INVALID
+    big = dict(B=2048, L_stride=4096, k=64)   # the rerank's lists alone: 2048 * 1024 * 64 * 8 bytes
+    assert lib.adapld_workspace_bytes(7, 2048, 4096, 128, 64, 20, 8, 2, 128) > cap
+    assert f(*args(**big)) == WS_SMALL
