@@ -379,6 +379,70 @@ def measure_paper_tree(adapld, cfg, bufs, s, tokens, lens, x, steps, stream):
                     "in place of the ranked-list tree; back-to-back calls; not part of the step"}
 
 
+def measure_ngram(adapld, cfg, x, steps, stream):
+    """The incremental n-gram index next to the whole-context lexical scan.
+    Contexts of the workload get room for `iters` iterations that each append
+    4 tokens (copied from earlier positions, so long suffix matches recur);
+    an iteration on the index path is adapld_ngram_index_append_match (the
+    new positions inserted, then the match, one launch), on the scan path
+    adapld_lexical_match.  Both
+    loops run back to back behind a spin kernel; the build is timed once."""
+    import torch
+    B, L, n_max = cfg.B, cfg.L, cfg.n_max
+    iters = max(steps, 20)
+    m = 4
+    cap = L + m * iters
+    rng = np.random.default_rng(77)
+    tok = np.zeros((B, cap), np.int32)
+    tok[:, :L] = x["tokens"]
+    lens0 = np.clip(x["lens"], 0, L).astype(np.int32)
+    for b in range(B):
+        for i in range(iters):
+            at = int(lens0[b]) + m * i
+            src = int(rng.integers(0, max(at - m, 1)))
+            tok[b, at:at + m] = tok[b, src:src + m]
+    tok_d = torch.from_numpy(tok).cuda()
+    lens_seq = [torch.from_numpy(lens0 + m * (i + 1)).cuda() for i in range(iters)]
+    lens_0 = torch.from_numpy(lens0).cuda()
+    idx = adapld.NgramIndex(B, cap, n_max)
+    out = [torch.empty((B, cap), dtype=torch.int32, device="cuda"), torch.empty(B, dtype=torch.int32, device="cuda"),
+           torch.empty(B, dtype=torch.int32, device="cuda")]
+
+    def timed(fn, n):
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(int(n * 60e3))
+        e0.record(stream)
+        for i in range(n):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e3
+
+    build_us = timed(lambda i: idx.build(tok_d, lens_0), 1)
+    index_us = timed(lambda i: idx.append_match(tok_d, lens_seq[i], cand_pos=out[0], cand_count=out[1],
+                                                match_n=out[2]), iters)
+    # the last iteration's answer against the scan's on the same context
+    sp, sc, sn = adapld.lexical_match(tok_d, lens_seq[-1], n_max)
+    same = bool(torch.equal(sc, out[1]) and torch.equal(sn, out[2]))
+    if same:
+        for b in range(B):
+            c = int(sc[b])
+            same = same and bool(torch.equal(sp[b, :c], out[0][b, :c]))
+    match_us = timed(lambda i: idx.match(tok_d, lens_seq[-1], cand_pos=out[0], cand_count=out[1], match_n=out[2]),
+                     iters)
+    scan_us = timed(lambda i: adapld.lexical_match(tok_d, lens_seq[i], n_max, cand_pos=out[0], cand_count=out[1],
+                                                   match_n=out[2]), iters)
+    nbytes = idx.buf.numel()
+    del idx, tok_d, lens_seq, out
+    return {"call": "adapld_ngram_index_append_match", "iteration_us": index_us,
+            "match_only_us": match_us, "lexical_scan_us": scan_us, "build_us": build_us,
+            "tokens_appended_per_iteration": m, "iterations": iters, "index_bytes": nbytes,
+            "same_as_scan": same,
+            "note": "the index path in place of the lexical scan, back-to-back iterations; not part of the step"}
+
+
 def measure(adapld, cfg, name, make_inputs, args):
     import torch
     log(f"[bench] generating {name}")
@@ -509,8 +573,9 @@ def measure(adapld, cfg, name, make_inputs, args):
         graph_us = g0.elapsed_time(g1) / steps * 1e3
         del graphs
 
-    acc = emb = ptree = None
+    acc = emb = ptree = ngram = None
     if not args.no_extras:
+        ngram = measure_ngram(adapld, cfg, x, steps, stream)
         acc = measure_accept(adapld, cfg, bufs, sets[0], x["lens"], lens, node_count, steps, stream)
         emb = measure_embed(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
         ptree = measure_paper_tree(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
@@ -558,6 +623,7 @@ def measure(adapld, cfg, name, make_inputs, args):
         "accept": acc,
         "embedding_fallback": emb,
         "paper_tree": ptree,
+        "ngram_index": ngram,
     }
     del sets, bufs
     torch.cuda.empty_cache()

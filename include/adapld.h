@@ -418,6 +418,55 @@ int adapld_semantic_topk_embed(const uint16_t* bank, const uint16_t* query, cons
                                void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Incremental n-gram index -- the lexical anchoring of adapld_lexical_match
+ * (Sec. 3.3, the exact-match set generalised to the longest matching suffix
+ * n-gram) answered from a device-resident index that is brought up to date
+ * with each iteration's new tokens, instead of a scan of the whole context
+ * (the draft-search cost trade-off of Appendix E, "Boundary Conditions for
+ * Effective Reuse").
+ *
+ * For every sequence and n = 1 .. n_max the index keeps, for each n-gram that
+ * ends at a candidate position j in [n-1, L-2], the ascending array of those
+ * positions.  adapld_ngram_index_match then returns exactly what
+ * adapld_lexical_match returns for the current tokens and lens (same outputs,
+ * bit for bit), reading C_lex as one contiguous array.
+ *
+ *   tokens, lens, B, L_stride, n_max   as in adapld_lexical_match; every call
+ *              on one index uses the same B, L_stride and n_max
+ *   index      caller-owned device buffer of adapld_ngram_index_bytes(B,
+ *              L_stride, n_max) bytes, 16-byte aligned; it holds the index
+ *              between calls (the one piece of state the library keeps, in
+ *              the caller's memory)
+ *
+ * adapld_ngram_index_build   indexes the current contexts from scratch.
+ * adapld_ngram_index_append  brings the index up to date after tokens were
+ *              appended to the contexts (tokens[b, L_old .. L-1] written,
+ *              lens[b] raised): it inserts only the positions that became
+ *              candidates, j in [L_old - 1, L - 2].  A sequence whose length
+ *              went down, or an index that was never built, is rebuilt.
+ * adapld_ngram_index_match   cand_pos / cand_count / match_n as
+ *              adapld_lexical_match; a sequence whose index does not reflect
+ *              lens[b] (append not called) gets match_n = -1, cand_count = 0.
+ * adapld_ngram_index_append_match  append, then match, in one launch (one
+ *              iteration of the decoding loop's lexical step).
+ *
+ * Errors: NULL_ARG; INVALID_ARG (B < 0, L_stride < 1, misaligned index);
+ * UNSUPPORTED (n_max outside 1..ADAPLD_MAX_NMAX, B > 65535, L_stride >
+ * 2^24); WORKSPACE_TOO_SMALL (index_bytes below the size).
+ */
+size_t adapld_ngram_index_bytes(int B, int L_stride, int n_max);
+int adapld_ngram_index_build(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                             void* index, size_t index_bytes, hipStream_t stream);
+int adapld_ngram_index_append(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                              void* index, size_t index_bytes, hipStream_t stream);
+int adapld_ngram_index_match(const int32_t* tokens, const int32_t* lens, const void* index, size_t index_bytes,
+                             int B, int L_stride, int n_max, int32_t* cand_pos, int32_t* cand_count,
+                             int32_t* match_n, hipStream_t stream);
+int adapld_ngram_index_append_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                                    void* index, size_t index_bytes, int32_t* cand_pos, int32_t* cand_count,
+                                    int32_t* match_n, hipStream_t stream);
+
+/*
  * adapld_accept_greedy -- greedy verification of the draft tree (Sec. 3.6:
  * verification follows the standard speculative-decoding rule; Appendix C:
  * with greedy decoding a draft token is kept when it equals the target's own

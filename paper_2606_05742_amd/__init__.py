@@ -7,6 +7,6 @@ fallback.
 """
 from .binding import (  # noqa: F401
     KIND_LEX, KIND_NONE, KIND_SEM, SUCC_EVERY_BRANCH, SUCC_SEMANTIC_ONLY, AdapldError, StepBuffers, accept_greedy, build_draft_tree, build_draft_tree_paper,
-    StepCall, lexical_match, load_library, semantic_topk, semantic_topk_embed, step, step_calls, tree_verify_attn,
+    NgramIndex, StepCall, lexical_match, load_library, semantic_topk, semantic_topk_embed, step, step_calls, tree_verify_attn,
     verify_plan, workspace_bytes,
 )

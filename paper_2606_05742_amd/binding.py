@@ -67,6 +67,15 @@ SIGNATURES = {
                                       + [ctypes.c_int] + [ctypes.c_void_p] + [ctypes.c_int] * 3
                                       + [ctypes.c_void_p, ctypes.c_int, ctypes.c_float] + [ctypes.c_int] * 3
                                       + [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p]),
+    "adapld_ngram_index_bytes": (ctypes.c_size_t, [ctypes.c_int] * 3),
+    "adapld_ngram_index_build": (ctypes.c_int, [ctypes.c_void_p] * 2 + [ctypes.c_int] * 3
+                                 + [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "adapld_ngram_index_append": (ctypes.c_int, [ctypes.c_void_p] * 2 + [ctypes.c_int] * 3
+                                  + [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "adapld_ngram_index_match": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_size_t] + [ctypes.c_int] * 3
+                                 + [ctypes.c_void_p] * 4),
+    "adapld_ngram_index_append_match": (ctypes.c_int, [ctypes.c_void_p] * 2 + [ctypes.c_int] * 3
+                                        + [ctypes.c_void_p, ctypes.c_size_t] + [ctypes.c_void_p] * 4),
     "adapld_tree_verify_attn": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -347,6 +356,62 @@ def accept_greedy(node_token, node_parent, node_depth, node_count, tree_mask, ta
         _stream(stream))
     _check(st, "adapld_accept_greedy")
     return accept_len, accept_nodes, out_tokens
+
+
+class NgramIndex:
+    """The incremental n-gram index of B contexts of capacity L_stride
+    (adapld_ngram_index_*): build once, append after the contexts grow, match
+    in place of lexical_match.  Holds the index's device buffer."""
+
+    def __init__(self, B, L_stride, n_max, device="cuda"):
+        self.B, self.L_stride, self.n_max = B, L_stride, n_max
+        nbytes = load_library().adapld_ngram_index_bytes(B, L_stride, n_max)
+        if nbytes == 0:
+            raise AdapldError(-2, f"no index for B={B}, L_stride={L_stride}, n_max={n_max}")
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+    def _args(self, tokens, lens):
+        i32 = (torch.int32,)
+        return (_ptr(tokens, "tokens", i32, (self.B, self.L_stride)), _ptr(lens, "lens", i32, (self.B,)))
+
+    def build(self, tokens, lens, stream=None):
+        st = load_library().adapld_ngram_index_build(*self._args(tokens, lens), self.B, self.L_stride, self.n_max,
+                                                     self.buf.data_ptr(), self.buf.numel(), _stream(stream))
+        _check(st, "adapld_ngram_index_build")
+        return self
+
+    def append(self, tokens, lens, stream=None):
+        st = load_library().adapld_ngram_index_append(*self._args(tokens, lens), self.B, self.L_stride, self.n_max,
+                                                      self.buf.data_ptr(), self.buf.numel(), _stream(stream))
+        _check(st, "adapld_ngram_index_append")
+        return self
+
+    def _outs(self, dev, cand_pos, cand_count, match_n):
+        B, Ls = self.B, self.L_stride
+        cand_pos = torch.empty((B, Ls), dtype=torch.int32, device=dev) if cand_pos is None else cand_pos
+        cand_count = _i32(B, dev) if cand_count is None else cand_count
+        match_n = _i32(B, dev) if match_n is None else match_n
+        i32 = (torch.int32,)
+        ptrs = (_ptr(cand_pos, "cand_pos", i32, (B, Ls)), _ptr(cand_count, "cand_count", i32, (B,)),
+                _ptr(match_n, "match_n", i32, (B,)))
+        return (cand_pos, cand_count, match_n), ptrs
+
+    def match(self, tokens, lens, *, cand_pos=None, cand_count=None, match_n=None, stream=None):
+        """(cand_pos, cand_count, match_n), as lexical_match returns them."""
+        outs, ptrs = self._outs(tokens.device, cand_pos, cand_count, match_n)
+        st = load_library().adapld_ngram_index_match(*self._args(tokens, lens), self.buf.data_ptr(), self.buf.numel(),
+                                                     self.B, self.L_stride, self.n_max, *ptrs, _stream(stream))
+        _check(st, "adapld_ngram_index_match")
+        return outs
+
+    def append_match(self, tokens, lens, *, cand_pos=None, cand_count=None, match_n=None, stream=None):
+        """append, then match, in one launch."""
+        outs, ptrs = self._outs(tokens.device, cand_pos, cand_count, match_n)
+        st = load_library().adapld_ngram_index_append_match(*self._args(tokens, lens), self.B, self.L_stride,
+                                                            self.n_max, self.buf.data_ptr(), self.buf.numel(), *ptrs,
+                                                            _stream(stream))
+        _check(st, "adapld_ngram_index_append_match")
+        return outs
 
 
 @dataclass

@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libadapld.so")
 
-SOURCES = ["lexical.hip", "semantic.hip", "tree.hip", "paper_tree.hip", "verify.hip", "accept.hip", "embed.hip", "noalloc.hip", "abi.cpp"]
+SOURCES = ["lexical.hip", "semantic.hip", "tree.hip", "paper_tree.hip", "verify.hip", "accept.hip", "embed.hip", "ngram.hip", "noalloc.hip", "abi.cpp"]
 ARCH = "gfx950"
 
 # -packed-fp32-ops keeps the compiler from emitting packed fp32 VALU ops.

@@ -9,7 +9,7 @@ namespace {
 
 thread_local int g_last_hip_error = 0;
 
-constexpr int kVersion = 10300;  // 1.3.0: adapld_step_noalloc
+constexpr int kVersion = 10400;  // 1.4.0: the incremental n-gram index
 
 bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
@@ -330,6 +330,66 @@ int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank
                                         L_stride, T_max, Hq, Hkv, scale, out, lse, ws_ver,
                                         adapld::plan_verify(B, L_stride, T_max, Hq, Hkv), stream);
   return hip_status(e);
+}
+
+size_t adapld_ngram_index_bytes(int B, int L_stride, int n_max) {
+  if (B <= 0 || L_stride <= 0 || n_max < 1 || n_max > ADAPLD_MAX_NMAX) return 0;
+  return (size_t)B * n_max * adapld::ngram_level_bytes(L_stride);
+}
+
+}  // extern "C"
+
+namespace {
+
+int check_ngram(const int32_t* tokens, const int32_t* lens, const void* index, size_t index_bytes, int B,
+                int L_stride, int n_max) {
+  if (B < 0) return ADAPLD_ERR_INVALID_ARG;
+  if (B == 0) return ADAPLD_OK;
+  if (!tokens || !lens || !index) return ADAPLD_ERR_NULL_ARG;
+  if (L_stride < 1 || misaligned16(index)) return ADAPLD_ERR_INVALID_ARG;
+  if (n_max < 1 || n_max > ADAPLD_MAX_NMAX || B > 65535 || L_stride > (1 << 24))
+    return ADAPLD_ERR_UNSUPPORTED;
+  if (index_bytes < adapld_ngram_index_bytes(B, L_stride, n_max)) return ADAPLD_ERR_WORKSPACE_TOO_SMALL;
+  return ADAPLD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int adapld_ngram_index_build(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                             void* index, size_t index_bytes, hipStream_t stream) {
+  if (const int st = check_ngram(tokens, lens, index, index_bytes, B, L_stride, n_max); st != ADAPLD_OK || B == 0)
+    return st;
+  return hip_status(adapld::launch_ngram_update(tokens, lens, B, L_stride, n_max, index, 1, stream));
+}
+
+int adapld_ngram_index_append(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                              void* index, size_t index_bytes, hipStream_t stream) {
+  if (const int st = check_ngram(tokens, lens, index, index_bytes, B, L_stride, n_max); st != ADAPLD_OK || B == 0)
+    return st;
+  return hip_status(adapld::launch_ngram_append(tokens, lens, B, L_stride, n_max, index, nullptr, nullptr, nullptr,
+                                                stream));
+}
+
+int adapld_ngram_index_append_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                                    void* index, size_t index_bytes, int32_t* cand_pos, int32_t* cand_count,
+                                    int32_t* match_n, hipStream_t stream) {
+  if (const int st = check_ngram(tokens, lens, index, index_bytes, B, L_stride, n_max); st != ADAPLD_OK || B == 0)
+    return st;
+  if (!cand_pos || !cand_count || !match_n) return ADAPLD_ERR_NULL_ARG;
+  return hip_status(adapld::launch_ngram_append(tokens, lens, B, L_stride, n_max, index, cand_pos, cand_count,
+                                                match_n, stream));
+}
+
+int adapld_ngram_index_match(const int32_t* tokens, const int32_t* lens, const void* index, size_t index_bytes,
+                             int B, int L_stride, int n_max, int32_t* cand_pos, int32_t* cand_count,
+                             int32_t* match_n, hipStream_t stream) {
+  if (const int st = check_ngram(tokens, lens, index, index_bytes, B, L_stride, n_max); st != ADAPLD_OK || B == 0)
+    return st;
+  if (!cand_pos || !cand_count || !match_n) return ADAPLD_ERR_NULL_ARG;
+  return hip_status(adapld::launch_ngram_match(tokens, lens, index, B, L_stride, n_max, cand_pos, cand_count,
+                                               match_n, stream));
 }
 
 int adapld_accept_greedy(const int32_t* node_token, const int32_t* node_parent,

@@ -49,6 +49,23 @@ size_t verify_ws_bytes(const VerifyPlan& p, int B, int Hkv);
 // ADAPLD_ERR_HIP.
 int record_hip_error(hipError_t e);
 
+// Incremental n-gram index: per (sequence, n-gram length) level, a table of
+// 16-byte slots (a power of two, at least twice the context capacity), a
+// pool of position arrays and a 16-byte header.
+__host__ __device__ inline size_t ngram_slots(int L_stride) {
+  size_t s = 16;
+  while (s < 2 * (size_t)L_stride) s <<= 1;
+  return s;
+}
+// Every array's capacity is a power of two >= 4 that doubles when full, so an
+// array of c positions has used at most max(8, 4c) ints over its life: the
+// pool never needs more than 8 per n-gram plus 4 per position, 12 per token.
+__host__ __device__ inline size_t ngram_pool_ints(int L_stride) { return 12 * (size_t)L_stride + 16; }
+__host__ __device__ inline size_t ngram_level_bytes(int L_stride) {
+  const size_t n = ngram_slots(L_stride) * 16 + ngram_pool_ints(L_stride) * 4 + 16;
+  return (n + 255) / 256 * 256;
+}
+
 // ---------------------------------------------------------------- launchers
 // Each returns the hipError_t of its launches (hipSuccess on success).
 hipError_t launch_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int L_stride,
@@ -121,6 +138,18 @@ hipError_t launch_successor_embed(const int32_t* tokens, const int32_t* lens, co
                                   int B, int W, int L_stride, int d, float tau, const int32_t* skip,
                                   const int32_t* branch_tok, uint8_t* flags, int32_t* lists,
                                   int32_t* counts, hipStream_t stream);
+
+// Builds (rebuild = 1) or brings up to date (0) the n-gram index of every
+// sequence; then answers the lexical match from it.
+hipError_t launch_ngram_update(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max,
+                               void* index, int rebuild, hipStream_t stream);
+// Brings the index up to date after appends; with cand_pos also answers the
+// lexical match in the same launch.
+hipError_t launch_ngram_append(const int32_t* tokens, const int32_t* lens, int B, int L_stride, int n_max, void* index,
+                               int32_t* cand_pos, int32_t* cand_count, int32_t* match_n, hipStream_t stream);
+hipError_t launch_ngram_match(const int32_t* tokens, const int32_t* lens, const void* index, int B, int L_stride,
+                              int n_max, int32_t* cand_pos, int32_t* cand_count, int32_t* match_n,
+                              hipStream_t stream);
 
 hipError_t launch_accept_greedy(const int32_t* node_token, const int32_t* node_parent,
                                 const int32_t* node_depth, const int32_t* node_count,

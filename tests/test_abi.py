@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 19
     for n in names:
         assert hasattr(lib, n), n
         assert n in binding.SIGNATURES, n
@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(lib):
 def test_status_strings(lib):
     for code in (OK, NULL, INVALID, UNSUPPORTED, WS_SMALL, -5, 123):
         assert lib.adapld_status_string(code)
-    assert lib.adapld_version() == 10300
+    assert lib.adapld_version() == 10400
     assert lib.adapld_last_hip_error() == 0
 
 
@@ -267,3 +267,27 @@ def test_step_noalloc_validation(lib):
     big = dict(B=2048, L_stride=4096, k=64)   # the rerank's lists alone: 2048 * 1024 * 64 * 8 bytes
     assert lib.adapld_workspace_bytes(7, 2048, 4096, 128, 64, 20, 8, 2, 128) > cap
     assert f(*args(**big)) == WS_SMALL
+
+
+def test_ngram_index_validation(lib):
+    """Host checks of the n-gram index calls (nothing is launched)."""
+    need = lib.adapld_ngram_index_bytes(2, 64, 4)
+    assert need > 0 and lib.adapld_ngram_index_bytes(2, 64, 65) == 0 and lib.adapld_ngram_index_bytes(0, 64, 4) == 0
+    for f in (lib.adapld_ngram_index_build, lib.adapld_ngram_index_append):
+        assert f(P, P, 0, 64, 4, P, need, N) == OK
+        assert f(P, P, -1, 64, 4, P, need, N) == INVALID
+        assert f(N, P, 2, 64, 4, P, need, N) == NULL
+        assert f(P, P, 2, 64, 4, N, need, N) == NULL
+        assert f(P, P, 2, 0, 4, P, need, N) == INVALID
+        assert f(P, P, 2, 64, 0, P, need, N) == UNSUPPORTED
+        assert f(P, P, 2, 64, 65, P, need, N) == UNSUPPORTED
+        assert f(P, P, 2, 64, 4, ctypes.c_void_p(0x10008), need, N) == INVALID
+        assert f(P, P, 2, 64, 4, P, need - 1, N) == WS_SMALL
+    am = lib.adapld_ngram_index_append_match
+    assert am(P, P, 0, 64, 4, P, need, P, P, P, N) == OK
+    assert am(P, P, 2, 64, 4, P, need, P, N, P, N) == NULL
+    assert am(P, P, 2, 1 << 25, 4, P, 1 << 60, P, P, P, N) == UNSUPPORTED
+    m = lib.adapld_ngram_index_match
+    assert m(P, P, P, need, 0, 64, 4, P, P, P, N) == OK
+    assert m(P, P, P, need, 2, 64, 4, N, P, P, N) == NULL
+    assert m(P, P, P, need - 1, 2, 64, 4, P, P, P, N) == WS_SMALL
