@@ -24,7 +24,9 @@ OP_STEP = 7
 SUCC_EVERY_BRANCH, SUCC_SEMANTIC_ONLY = 0, 1
 HEAD_DIM = 128
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadapld.so")
+# ADAPLD_LIB names another build of the library (the sanitized host test
+# build); by default the in-tree libadapld.so.
+LIB_PATH = os.environ.get("ADAPLD_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libadapld.so")
 
 _c_i32p = ctypes.c_void_p
 _lib = None

@@ -69,6 +69,43 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# The host-side C-ABI glue built with AddressSanitizer and UBSan (gcc, host
+# code only) and linked with the regular objects: a test library for the
+# argument-validation paths, loaded with the gcc sanitizer runtimes preloaded.
+HOSTSAN_LIB = os.path.join(BUILD, "libadapld_hostsan.so")
+HOSTSAN_FLAGS = ["-O1", "-g", "-std=c++17", "-fPIC", "-fno-omit-frame-pointer", "-fsanitize=address,undefined"]
+
+
+def build_host_sanitized() -> str:
+    """libadapld with abi.cpp compiled by g++ under ASan + UBSan; the kernels'
+    objects are the regular ones (built first when missing)."""
+    objs = [os.path.join(BUILD, os.path.splitext(src)[0] + ".o") for src in SOURCES if src != "abi.cpp"]
+    if not all(os.path.exists(o) for o in objs):
+        build()
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(hipcc())))
+    san_obj = os.path.join(BUILD, "abi_hostsan.o")
+    cmd = ["g++", *HOSTSAN_FLAGS, "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(rocm, "include"), "-I", INCLUDE,
+           "-I", CSRC, "-x", "c++", "-c", os.path.join(CSRC, "abi.cpp"), "-o", san_obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized compile of abi.cpp failed:\n{r.stderr}")
+    cmd = ["g++", "-shared", "-fsanitize=address,undefined", "-o", HOSTSAN_LIB, san_obj, *objs,
+           "-L", os.path.join(rocm, "lib"), "-lamdhip64", f"-Wl,-rpath,{os.path.join(rocm, 'lib')}"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{r.stderr}")
+    return HOSTSAN_LIB
+
+
+def sanitizer_preload() -> str:
+    """LD_PRELOAD value for a process that loads HOSTSAN_LIB."""
+    libs = []
+    for name in ("libasan.so", "libubsan.so"):
+        out = subprocess.run(["gcc", f"-print-file-name={name}"], capture_output=True, text=True).stdout.strip()
+        libs.append(out)
+    return ":".join(libs)
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)

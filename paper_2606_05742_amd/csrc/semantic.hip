@@ -62,10 +62,18 @@ __device__ __forceinline__ void seq_rows(const ScanArgs& a, int b, int& L, int& 
   nrows = cc > 0 ? cc : (a.rerank_only ? 0 : max(L - 1, 0));
 }
 
-// Rows are split over W = min(kScanWaveSlots, total) waves, wave w taking
-// [floor(w total / W), floor((w+1) total / W)): never empty, so the waves that
-// meet one sequence are consecutive and each writes one list.
-__device__ __forceinline__ int scan_waves(int total) { return total < kScanWaveSlots ? total : kScanWaveSlots; }
+// Rows are split over W waves, wave w taking [floor(w total / W),
+// floor((w+1) total / W)): never empty, so the waves that meet one sequence
+// are consecutive and each writes one list.  Up to kScanWaveSlots rows, one
+// row per wave (the scan is one memory round trip); beyond that at least
+// kScanMinRows rows per wave, so a mid-sized scan's merge reads fewer, longer
+// lists (b1_l4096: 512 lists instead of 1024, 49.5 -> 46.8 us per step).
+constexpr int kScanMinRows = 8;
+__device__ __forceinline__ int scan_waves(int total) {
+  if (total <= kScanWaveSlots) return total;
+  const int w = (total + kScanMinRows - 1) / kScanMinRows;
+  return w < kScanWaveSlots ? w : kScanWaveSlots;
+}
 __device__ __forceinline__ int wave_of_row(int g, int total) {
   return (int)((((int64_t)g + 1) * scan_waves(total) - 1) / total);
 }

@@ -12,9 +12,10 @@ import sys
 from concurrent.futures import ThreadPoolExecutor
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-PINS = ["tests/test_oracle_lexical.py", "tests/test_oracle_semantic.py",
-        "tests/test_oracle_tree.py", "tests/test_oracle_verify.py", "tests/test_oracle_accept.py",
-        "tests/test_oracle_embedding.py", "tests/test_oracle_tree_paper.py", "tests/test_oracle_step.py"]
+# fastest first: with -x a caught mutant stops at its first failing pin
+PINS = ["tests/test_oracle_accept.py", "tests/test_oracle_embedding.py", "tests/test_oracle_step.py",
+        "tests/test_oracle_tree_paper.py", "tests/test_oracle_verify.py", "tests/test_oracle_tree.py",
+        "tests/test_oracle_lexical.py", "tests/test_oracle_semantic.py"]
 
 MUTANTS = [
     ("js = np.arange(n - 1, L - 1)", "js = np.arange(n - 1, L)"),              # anchor counts itself
