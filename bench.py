@@ -30,8 +30,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "c45dde192fd12fa736af5171b2a1624f893ad8834415bb7a1b5de37e140f77f2",
-    "fetch_kib": 269412.9,
+    "source_sha256": "7320d849a1cd5faf5861a900b629e9088a0f0a720faac2b5f38644294ad3b719",
+    "fetch_kib": 267563.0,
     "write_kib": 5392.1,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
