@@ -339,21 +339,32 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
   const int k = a.k;
   const uint64_t* __restrict__ lists = a.ws_keys + (size_t)b * a.lists * k;
 
-  uint64_t th = 0;
-  for (int c = threadIdx.x; c < nvalid; c += kScanThreads) {
-    const uint64_t v = lists[(size_t)c * k + (k - 1)];
-    th = v > th ? v : th;
+  // Two lower bounds on the final k-th key, whose loads go out together: the
+  // largest k-th entry over the lists (that list alone has k keys above it),
+  // and the k-th largest of 64 per-lane maxima of list heads in wave 0 (lane l
+  // takes lists l, l+64, ..., l+448; at least k heads reach it).
+  // Loads are batched and branch-free (indices clamped into the lists, the
+  // excess masked afterwards), so a batch is one memory round trip.
+  uint64_t th = 0, y = 0;
+  const bool heads = wave == 0 && nvalid >= k;
+  uint64_t h[8];
+  if (heads) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = lists[(size_t)min(lane + j * kWave, nvalid - 1) * k];
+  }
+  for (int c0 = threadIdx.x; c0 < nvalid; c0 += 4 * kScanThreads) {
+    uint64_t v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = lists[(size_t)min(c0 + j * kScanThreads, nvalid - 1) * k + (k - 1)];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) th = (c0 + j * kScanThreads < nvalid && v[j] > th) ? v[j] : th;
+  }
+  if (heads) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) y = (lane + j * kWave < nvalid && h[j] > y) ? h[j] : y;
   }
   th = wave_max_u64(th);
   if (wave == 0 && nvalid >= k) {
-    // Lane l takes the largest head of lists l, l+64, ..., l+448; the k-th
-    // largest of these 64 maxima is reached by at least k heads, so it bounds
-    // the final k-th key from below.
-    uint64_t y = 0;
-    for (int c = lane; c < nvalid && c < 8 * kWave; c += kWave) {
-      const uint64_t h = lists[(size_t)c * k];
-      y = h > y ? h : y;
-    }
     y = bitonic_sort_desc(y);
     const uint64_t thb = readlane_u64(y, k - 1);
     th = thb > th ? thb : th;
@@ -364,16 +375,32 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
 #pragma unroll
   for (int w = 0; w < kScanWaves; ++w) th = s_red[w] > th ? s_red[w] : th;
   const uint64_t floor_key = th > 0 ? th : 1;  // key 0 marks an empty slot
-  for (int i = threadIdx.x; i < nvalid * k; i += kScanThreads) {
-    const uint64_t v = lists[i];
-    if (v >= floor_key) {
-      const int slot = atomicAdd(&s_ncand, 1);
-      if (slot < kMaxCand) s_cand[slot] = v;
-    }
+  const int nkeys = nvalid * k;
+  for (int i0 = threadIdx.x; i0 < nkeys; i0 += 8 * kScanThreads) {
+    uint64_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = lists[min(i0 + j * kScanThreads, nkeys - 1)];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (i0 + j * kScanThreads < nkeys && v[j] >= floor_key) {
+        const int slot = atomicAdd(&s_ncand, 1);
+        if (slot < kMaxCand) s_cand[slot] = v[j];
+      }
   }
   __syncthreads();
   if (wave != 0) return;
   const int ncand = s_ncand;
+  // The tree (step only) reads the tokens after the ranked rows.  Requesting
+  // the lines after the first 64 gathered keys now, before the sort, lets the
+  // tree's reads hit this CU's cache instead of waiting on memory afterwards.
+  int pf0 = 0, pf1 = 0;
+  const bool prefetch = tree.tokens != nullptr && lane < ncand && L >= 2;
+  if (prefetch) {
+    const int32_t* M = tree.tokens + (size_t)b * a.L_stride;
+    const int p = min(max(key_pos(s_cand[lane]), 0), L - 2);
+    pf0 = M[p + 1];
+    pf1 = M[min(p + 1 + tree.S, L - 1)];
+  }
   uint64_t mine = 0;
   if (ncand <= kMaxCand) {
     for (int base = 0; base < ncand; base += kWave) {
@@ -387,6 +414,9 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
     }
   }
 
+  // Consumes the prefetched tokens, which keeps the loads and places their
+  // wait here (s_ncand is not read again, so the store is harmless).
+  if (prefetch && (pf0 | pf1) == -1) s_ncand = -1;
   const float score = key_score(mine);
   bool keep = lane < k && mine != 0ull;
   if (cc == 0 && !isnan(tau)) keep = keep && score >= tau;  // tau filters the fallback only

@@ -218,10 +218,17 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
     for (int ds = 0; ds < kD / 16; ++ds)
       qf[nb][ds] = as_bf16x8(valid ? *reinterpret_cast<const uint4*>(qp + 16 * ds) : make_uint4(0, 0, 0, 0));
   }
-  if (do_tree)
-    for (int i = threadIdx.x; i < T * a.nw; i += kThreads) s_mask[i] = a.tree_mask[(size_t)b * a.T_max * a.nw + i];
-  waitcnt_vm<0>();   // the query loads retire here, on every path, before the pipeline starts
-  __syncthreads();   // mask table visible
+  // The tree's mask rows go to registers here and to LDS once every load of
+  // the prologue has landed (below), so they share one memory round trip with
+  // the query loads and the first tiles.
+  constexpr int kMaskRegs = (ADAPLD_MAX_TREE_NODES * kMaskWords + kThreads - 1) / kThreads;
+  const int n_mask = do_tree ? T * a.nw : 0;
+  uint64_t mw[kMaskRegs];
+#pragma unroll
+  for (int r = 0; r < kMaskRegs; ++r) {
+    const int i = threadIdx.x + r * kThreads;
+    mw[r] = i < n_mask ? a.tree_mask[(size_t)b * a.T_max * a.nw + i] : 0ull;
+  }
 
   float m_run[NB], l_run[NB];
   f32x16_t o[NB][kD / 32];
@@ -266,6 +273,19 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
                         lk, lv, wave, lane);
     }
   };
+  // The first kStages - 1 tiles are requested together with the query and
+  // mask loads above; all of them have landed after this wait (loads return
+  // in order), and the barrier publishes the tiles and the mask table.
+#pragma unroll
+  for (int t = 0; t < kStages - 1; ++t)
+    if (t < n_tiles) issue(t);
+  waitcnt_vm<0>();
+#pragma unroll
+  for (int r = 0; r < kMaskRegs; ++r) {
+    const int i = threadIdx.x + r * kThreads;
+    if (i < n_mask) s_mask[i] = mw[r];
+  }
+  __syncthreads();
 
   // Lane-dependent LDS byte offsets within a stage.  K fragment for dims
   // [16*ds + 8*half, +8) of key row kb*32 + col sits at kofs[ds] + kb*32*kRowBytes.
@@ -417,9 +437,6 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   const int H = HP * n_tiles;
   const int n_plain = max(c1 - c0, 0) / kKeyTile;   // leading context tiles with no masked key
   const int H_plain = HP * n_plain;
-#pragma unroll
-  for (int t = 0; t < kStages - 1; ++t)
-    if (t < n_tiles) issue(t);
   // A wave whose row block holds no valid row (the tail of the last row
   // group) issues its share of every tile and takes every barrier, and does
   // no math: its MFMAs would only cost power.
@@ -641,12 +658,14 @@ VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv) {
   // combine kernel when the context is split.  The constants are in units of
   // one SIMD's time for 32 rows x 64 keys with two waves per SIMD.
   constexpr double kStartTiles = 12.0;    // start-up and drain of one workgroup
-  constexpr double kCombineTiles = 10.0;  // the combine launch and its traffic
+  constexpr double kCombineTiles = 6.0;   // the combine launch and its traffic
   struct Cand { int waves, kh; double per_tile; };   // per_tile: SIMD cost of one 64-key tile
   const Cand cands[] = {{8, 1, 2.0}, {8, 2, 1.0}};
   const int G = Hq / Hkv;
   const int rows_max = T_max * G;
-  const int max_split = std::max(1, (L_stride + 4 * kKeyTile - 1) / (4 * kKeyTile));
+  // A split holds at least one tile; small grids (one short sequence) gain
+  // from splits of one or two tiles, since their time is mostly start-up.
+  const int max_split = std::min(64, std::max(1, (L_stride + kKeyTile - 1) / kKeyTile));
   VerifyPlan best{};
   double best_cost = 0.0;
   for (const Cand& c : cands) {
