@@ -18,8 +18,8 @@
 namespace adapld {
 
 
-// Called by every lane of one wave; s_start holds ADAPLD_MAX_TREE_NODES ints
-// of LDS that only this wave uses.
+// Called by every lane of one wave; s_start holds 2 * ADAPLD_MAX_TREE_NODES
+// ints of LDS that only this wave uses.
 __device__ __forceinline__ void build_tree_wave(const TreeOut& t, int b, int L_stride, int L, int r, int cnt,
                                                 int* s_start) {
   const int lane = lane_id();
@@ -45,20 +45,42 @@ __device__ __forceinline__ void build_tree_wave(const TreeOut& t, int b, int L_s
   const int T = __builtin_amdgcn_readlane(incl, kWave - 1);
 
   const size_t nb = (size_t)b * t.T_max;
+  // Every node's branch start and source row go to LDS; the nodes are then
+  // written 64 at a time across the lanes, with the token loads of all of
+  // them in flight together (a lane walking its own branch would wait for
+  // each token, and for its earlier stores, in turn).
+  int* s_row = s_start + ADAPLD_MAX_TREE_NODES;
   for (int dd = 0; dd < len; ++dd) {
-    const int u = start + dd;
-    t.node_token[nb + u] = M[r + 1 + dd];
-    t.node_parent[nb + u] = dd == 0 ? -1 : u - 1;
-    t.node_depth[nb + u] = dd;
-    t.node_src[nb + u] = r + 1 + dd;
-    s_start[u] = start;
+    s_start[start + dd] = start;
+    s_row[start + dd] = r;
   }
   if (lane == 0) t.node_count[b] = T;
-  // s_start is written and read by this wave only; its LDS operations
-  // complete in order, so a wave-level fence is enough.
+  // s_start and s_row are written and read by this wave only; its LDS
+  // operations complete in order, so a wave-level fence is enough.
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (T > 0) {
+    constexpr int kChunks = (ADAPLD_MAX_TREE_NODES + kWave - 1) / kWave;
+    int tok_u[kChunks], src_u[kChunks], dd_u[kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const int u = min(c * kWave + lane, T - 1);   // past T: a repeat of node T-1, not stored
+      dd_u[c] = u - s_start[u];
+      src_u[c] = s_row[u] + 1 + dd_u[c];             // <= L-1 by the branch length
+      tok_u[c] = M[src_u[c]];
+    }
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const int u = c * kWave + lane;
+      if (u < T) {
+        t.node_token[nb + u] = tok_u[c];
+        t.node_parent[nb + u] = dd_u[c] == 0 ? -1 : u - 1;
+        t.node_depth[nb + u] = dd_u[c];
+        t.node_src[nb + u] = src_u[c];
+      }
+    }
+  }
 
   const int nw = (t.T_max + 63) / 64;
   uint64_t* __restrict__ mrow = t.tree_mask + nb * nw;
