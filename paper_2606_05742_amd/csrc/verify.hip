@@ -424,6 +424,39 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
     }
     l_run[0] += psum;
   };
+  // Pieces of the same two steps for the unrolled loop below: the row max in
+  // log2 units, the rescale to a new max, and the exponentials of one 16-key
+  // part (s2) of the half, adding to psum in the order exp_pack uses.
+  auto row_max = [&](const f32x16_t& sv) {
+    float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
+#pragma unroll
+    for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, sv[r]), sv[r + 1]);
+    mx = fmaxf(mx, sv[15]);
+    const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_int(mx), __float_as_int(mx), false, false);
+    mx = fmaxf(__int_as_float(sw2[0]), __int_as_float(sw2[1]));
+    return mx * sl2;
+  };
+  auto rescale_to = [&](float mt) {
+    const float m_new = fmaxf(m_run[0], mt);
+    const float alpha = m_new == m_run[0] ? 1.f : __builtin_amdgcn_exp2f(m_run[0] - m_new);
+    m_run[0] = m_new;
+    l_run[0] *= alpha;
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db) o[0][db] *= alpha;
+  };
+  auto exp_part = [&](const f32x16_t& sv, int s2, float m_use, bf16x8_t& pbv, float& psum) {
+    bf16x8_t v;
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
+      const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[8 * s2 + i], sl2, -m_use));
+      const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[8 * s2 + i + 1], sl2, -m_use));
+      psum += p0 + p1;
+      const bf16x2_t pk = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
+      v[i] = pk[0];
+      v[i + 1] = pk[1];
+    }
+    pbv = v;
+  };
   // Before the first half of tile t+1: wait for its loads, then the barrier.
   // Every wave has passed the last read of tile t-1 by then, so its stage is
   // refilled with tile t+kStages-1.
@@ -469,13 +502,37 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
     // halves per stage, kStages stages) is the compile-time J: every LDS
     // address is then a lane offset plus an immediate.
     constexpr int kPeriod = HP * kStages;
+    // Its softmax is split so that each side of the tile barrier pairs eight
+    // MFMAs with about half of the VALU work: the exponentials of the first
+    // 16 keys go beside the MFMAs of P V (h-1), those of the last 16 beside
+    // the MFMAs of S (h+1).  They use the running max as it stands; the rare
+    // half whose max outgrows it by more than kRescaleSlack is recomputed
+    // after the check (the same values the check-first order gives).
     auto body_c = [&](auto J, int h) {
       constexpr int j = decltype(J)::value;
       pv_c(std::integral_constant<int, (j + kPeriod - 1) % kPeriod>{}, pb);
-      max_rescale(h, s_cur, std::false_type{});
+      const float mt = row_max(s_cur);
+      const float m_use = m_run[0] == -INFINITY ? 0.f : m_run[0];
+      float psum = 0.f;
+      bf16x8_t pn[2];
+      exp_part(s_cur, 0, m_use, pn[0], psum);
+      // Empty asm statements that consume the values pin each part to its
+      // side of the barrier: otherwise the compiler sinks both parts below
+      // the rescale check, whose rare branch does not need them.
+      asm volatile("" ::"v"(pn[0]), "v"(psum));
       if (j % HP == HP - 1 && h + 1 < H) next_tile(h / HP);
       qk_c(std::integral_constant<int, (j + 1) % kPeriod>{}, s_nxt);
-      exp_pack(s_cur, pb);
+      exp_part(s_cur, 1, m_use, pn[1], psum);
+      asm volatile("" ::"v"(pn[1]), "v"(psum));
+      if (__ballot(mt > m_run[0] + kRescaleSlack)) {
+        rescale_to(mt);
+        psum = 0.f;
+        exp_part(s_cur, 0, m_run[0], pn[0], psum);
+        exp_part(s_cur, 1, m_run[0], pn[1], psum);
+      }
+      l_run[0] += psum;
+      pb[0] = pn[0];
+      pb[1] = pn[1];
       s_cur = s_nxt;
     };
     using I1 = std::integral_constant<int, 1>;
