@@ -156,29 +156,41 @@ def cosine_rows(H: np.ndarray, rows, q: np.ndarray) -> np.ndarray:
     return out
 
 
-def semantic_topk(bank: np.ndarray, query, cand, k: int, tau=None):
+def semantic_topk(bank: np.ndarray, query, cand, k: int, tau=None, preceding=False):
     """Rank the retrieval candidates of one sequence.
 
-    bank: (L, d) float64 hidden states; query: (d,) float64 or None, meaning
-    the last bank row.  cand: the lexical candidate list (possibly empty).
-    With candidates (a lexical hit) the scored rows are the candidates and
-    kind = LEX; otherwise every row in [0, L-2] is scored (semantic fallback),
+    bank: (L, d) float64 hidden states; query: (d,) float64 or None.
+    cand: the lexical candidate list (possibly empty).  With candidates (a
+    lexical hit) the scored positions are the candidates and kind = LEX;
+    otherwise every position in [0, L-2] is a candidate (semantic fallback),
     entries below tau are dropped when tau is given, and kind = SEM if any
-    entry remains, else NONE.  Ranking: score descending, then position
-    ascending; the first min(k, #rows) are kept.
-    Returns (kind, positions, scores).
+    entry remains, else NONE.
+
+    The score of position j (Sec. 3.4, Eq. (6)):
+    - preceding=True, the equation as printed: the state before the candidate
+      against the state before the anchor, cos(H[j-1], q) with q = H[L-2] by
+      default; position 0 has no earlier state and is not scored (a lexical
+      hit whose only candidate is 0 keeps kind LEX with nothing ranked);
+    - preceding=False: cos(H[j], q) with q = H[L-1] by default (reading c.5).
+    Ranking: score descending, then position ascending; the first
+    min(k, #scored) are kept.  Returns (kind, positions, scores).
     """
     L = int(bank.shape[0])
-    q = bank[L - 1] if query is None else np.asarray(query, dtype=np.float64)
+    sh = 1 if preceding else 0
+    if query is not None:
+        q = np.asarray(query, dtype=np.float64)
+    else:
+        q = bank[L - 1 - sh] if L - 1 - sh >= 0 else np.zeros(bank.shape[1])
     if len(cand) > 0:
         rows = np.asarray(cand, dtype=np.int64)
         lexical = True
     else:
         rows = np.arange(0, max(L - 1, 0), dtype=np.int64)
         lexical = False
+    rows = rows[rows >= sh]
     if rows.size == 0:
-        return KIND_NONE, [], []
-    s = cosine_rows(bank, rows, q)
+        return (KIND_LEX if lexical else KIND_NONE), [], []
+    s = cosine_rows(bank, rows - sh, q)
     order = np.lexsort((rows, -s))
     top = order[: min(k, rows.size)]
     pos = [int(rows[i]) for i in top]
@@ -449,11 +461,12 @@ def compact_kv(kc_bits, vc_bits, kt_bits, vt_bits, L: int, path):
 
 def step(tokens, lens, bank_bits, query_bits, n_max, k, W, S, tau=None,
          q_bits=None, kc_bits=None, vc_bits=None, kt_bits=None, vt_bits=None,
-         scale=None, seqs=None, verify=True):
+         scale=None, seqs=None, verify=True, preceding=False):
     """Run the four steps for the sequences in ``seqs`` (default: all).
 
     tokens: (B, L_stride) int; lens: (B,); bank_bits: (B, L_stride, d) uint16;
-    query_bits: None (use row lens[b]-1) or (B, d) uint16.  Verify tensors are
+    query_bits: None (the default query of semantic_topk) or (B, d) uint16;
+    preceding: the score alignment of semantic_topk.  Verify tensors are
     bf16 bit patterns in the layouts Q (B, T_max, Hq, D), Kc/Vc
     (B, Hkv, L_stride, D), Kt/Vt (B, T_max, Hkv, D).  Returns one dict per
     sequence with every intermediate and output.
@@ -467,7 +480,7 @@ def step(tokens, lens, bank_bits, query_bits, n_max, k, W, S, tau=None,
         n_star, C = lexical_match(M, n_max)
         H = bf16_bits_to_f64(bank_bits[b, :L])
         qv = None if query_bits is None else bf16_bits_to_f64(query_bits[b])
-        kind, pos, sc = semantic_topk(H, qv, C, k, tau)
+        kind, pos, sc = semantic_topk(H, qv, C, k, tau, preceding=preceding)
         tree = build_draft_tree(M, kind, pos, W, S)
         rec = dict(b=b, n_star=n_star, cand=C, kind=kind, topk_pos=pos, topk_score=sc, tree=tree)
         if verify and tree["T"] > 0:

@@ -62,7 +62,14 @@ MUTANTS = [
     ("            sc_ = (1.0 / np.sqrt(Q.shape[-1])) if scale is None else scale",
      "            sc_ = (1.0 / Q.shape[-1]) if scale is None else scale"),
     ("        qv = None if query_bits is None else bf16_bits_to_f64(query_bits[b])", "        qv = None"),
-    ("        kind, pos, sc = semantic_topk(H, qv, C, k, tau)", "        kind, pos, sc = semantic_topk(H, qv, C, k, None)"),
+    ("        kind, pos, sc = semantic_topk(H, qv, C, k, tau, preceding=preceding)",
+     "        kind, pos, sc = semantic_topk(H, qv, C, k, None, preceding=preceding)"),
+    ("        kind, pos, sc = semantic_topk(H, qv, C, k, tau, preceding=preceding)",
+     "        kind, pos, sc = semantic_topk(H, qv, C, k, tau)"),                   # step ignores the alignment
+    ("    s = cosine_rows(bank, rows - sh, q)", "    s = cosine_rows(bank, rows, q)"),   # Eq. (6) rows not moved back
+    ("        q = bank[L - 1 - sh] if L - 1 - sh >= 0 else np.zeros(bank.shape[1])",
+     "        q = bank[L - 1] if L - 1 >= 0 else np.zeros(bank.shape[1])"),      # query not moved back
+    ("    rows = rows[rows >= sh]\n", ""),                                       # position 0 scored
     ("    seqs = range(B) if seqs is None else seqs", "    seqs = range(B)"),
     ("        main = list(range(j + 1, j + 1 + min(S + 1, L - 1 - j))) if kind == KIND_LEX else []",
      "        main = list(range(j + 1, j + 1 + min(S, L - 1 - j))) if kind == KIND_LEX else []"),

@@ -24,7 +24,7 @@ def test_golden_cases():
     for c in d["cases"]:
         H = np.array(d["banks"][c["bank"]], dtype=np.float64)
         q = None if c["query"] is None else np.array(c["query"], dtype=np.float64)
-        kind, pos, sc = semantic_topk(H, q, c["cand"], c["k"], c["tau"])
+        kind, pos, sc = semantic_topk(H, q, c["cand"], c["k"], c["tau"], preceding=c.get("preceding", False))
         assert kind == c["kind"] and pos == c["pos"], c
         np.testing.assert_allclose(sc, c["score"], rtol=0, atol=1e-15)
 
@@ -141,3 +141,47 @@ def test_planted_neighbour_ranks_first():
         # the noisy copy has cosine ~ 1/sqrt(1.01); unrelated N(0,1) rows ~ 0
         assert pos[0] in _copy_family(x["copy_logs"][i], src)
         assert sc[0] > 0.95
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_preceding_alignment_against_scipy(seed):
+    """Eq. (6) as printed, from SciPy: candidate j >= 1 scored by
+    1 - cosine distance(H[j-1], H[L-2]), ranked by repeated argmax."""
+    rng = np.random.default_rng(100 + seed)
+    L, d = 40, 12
+    base = rng.integers(-2, 3, size=(5, d)).astype(np.float64)
+    H = base[rng.integers(0, 5, size=L)]
+    H[rng.integers(0, L, size=3)] = 0.0
+    q = H[L - 2]
+
+    def sc(j):
+        return 0.0 if not H[j - 1].any() or not q.any() else 1.0 - scipy_cosine_distance(H[j - 1], q)
+
+    for k in (1, 4, 39):
+        rows = list(range(1, L - 1))
+        kind, pos, got = semantic_topk(H, None, [], k, None, preceding=True)
+        assert kind == KIND_SEM and pos == _argmax_select([sc(j) for j in rows], rows, k)
+        np.testing.assert_allclose(got, [sc(j) for j in pos], rtol=0, atol=1e-12)
+        cand = sorted(rng.choice(L - 1, size=8, replace=False).tolist())
+        kind, pos, _ = semantic_topk(H, None, cand, k, None, preceding=True)
+        kept = [c for c in cand if c >= 1]
+        assert kind == KIND_LEX and pos == _argmax_select([sc(j) for j in kept], kept, k)
+
+
+def test_preceding_is_the_row_alignment_one_step_back():
+    """Scoring H[j-1] equals scoring the rows of a bank moved down one row
+    (H'[j] = H[j-1]) with the default alignment, position 0 left out, and the
+    query H[L-2] passed explicitly."""
+    rng = np.random.default_rng(7)
+    L, d = 60, 9
+    H = rng.standard_normal((L, d))
+    Hs = np.vstack([rng.standard_normal((1, d)), H[:-1]])
+    # the fallback's candidates are every position 1..L-2 of the moved bank
+    a = semantic_topk(H, None, [], 6, None, preceding=True)
+    b = semantic_topk(Hs, H[L - 2], list(range(1, L - 1)), 6, None)
+    assert a[0] == KIND_SEM and a[1] == b[1]
+    np.testing.assert_allclose(a[2], b[2], rtol=0, atol=1e-15)
+    a = semantic_topk(H, None, [0, 5, 9, 30, 58], 6, None, preceding=True)
+    b = semantic_topk(Hs, H[L - 2], [5, 9, 30, 58], 6, None)
+    assert a[0] == KIND_LEX and a[1] == b[1]
+    assert semantic_topk(H, None, [0], 6, None, preceding=True) == (KIND_LEX, [], [])

@@ -38,13 +38,14 @@ def _batch(seed, B=4, L_stride=48, d=16, Hq=4, Hkv=2, D=8, W=3, S=2):
                 W=W, S=S, D=D)
 
 
-def _by_hand(x, b, n_max, k, tau, explicit_query, scale, verify):
+def _by_hand(x, b, n_max, k, tau, explicit_query, scale, verify, preceding=False):
     L = int(x["lens"][b])
     M = x["tokens"][b, :L]
     n_star, C = oracle.lexical_match(M, n_max)
     H = _decode(x["bank"][b, :L])
-    qv = _decode(x["query"][b]) if explicit_query else H[L - 1]
-    kind, pos, sc = oracle.semantic_topk(H, qv, C, k, tau)
+    # the default query: the anchor's own state, or (Eq. (6)) the one before it
+    qv = _decode(x["query"][b]) if explicit_query else H[L - 2 if preceding else L - 1]
+    kind, pos, sc = oracle.semantic_topk(H, qv, C, k, tau, preceding=preceding)
     tree = oracle.build_draft_tree(M, kind, pos, x["W"], x["S"])
     rec = dict(n_star=n_star, cand=C, kind=kind, topk_pos=pos, topk_score=sc, tree=tree)
     T = tree["T"]
@@ -56,19 +57,20 @@ def _by_hand(x, b, n_max, k, tau, explicit_query, scale, verify):
     return rec
 
 
+@pytest.mark.parametrize("preceding", [False, True])
 @pytest.mark.parametrize("explicit_query", [False, True])
 @pytest.mark.parametrize("tau", [None, 0.05])
-def test_step_equals_the_pinned_steps(explicit_query, tau):
+def test_step_equals_the_pinned_steps(explicit_query, tau, preceding):
     x = _batch(3)
     n_max, k = 3, 5
     seqs = [0, 2, 3]
     got = oracle.step(x["tokens"], x["lens"], x["bank"], x["query"] if explicit_query else None, n_max, k,
                       x["W"], x["S"], tau=tau, q_bits=x["q"], kc_bits=x["kc"], vc_bits=x["vc"],
-                      kt_bits=x["kt"], vt_bits=x["vt"], seqs=seqs)
+                      kt_bits=x["kt"], vt_bits=x["vt"], seqs=seqs, preceding=preceding)
     assert [r["b"] for r in got] == seqs
     kinds = set()
     for r in got:
-        want = _by_hand(x, r["b"], n_max, k, tau, explicit_query, 1.0 / np.sqrt(x["D"]), True)
+        want = _by_hand(x, r["b"], n_max, k, tau, explicit_query, 1.0 / np.sqrt(x["D"]), True, preceding)
         kinds.add(want["kind"])
         for key in ("n_star", "cand", "kind", "topk_pos"):
             assert r[key] == want[key], (r["b"], key)
