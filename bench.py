@@ -64,6 +64,8 @@ def log(msg):
 
 MFMA_PEAK_BF16_TFLOPS = 2500.0
 WARM_SECONDS = 1.0      # stepping before the timed steps, so that clocks have settled
+PRECEDING = True        # the rerank's alignment: Eq. (6) as printed (the states before the
+                        # candidate and before the anchor)
 SPREAD_BLOCKS = 9       # further blocks of K steps timed after the headline block
 
 
@@ -77,19 +79,26 @@ def hit_rates(kinds):
             "R_rec": n_sem / (n_sem + n_none) if n_sem + n_none else None, "N": N}
 
 
-def algorithmic_work(cfg, lens, cand_count, node_count, node_depth):
+def algorithmic_work(cfg, lens, cand_count, node_count, node_depth, first_cand=None):
     """Bytes and flops the method must move and compute per step, per kernel group.
 
     Each input byte is read once and each output byte written once.  Verify
     flops count 4*D per (query, key) pair over the context keys and the
-    ancestor-or-self tree keys of every node.
+    ancestor-or-self tree keys of every node.  With the Eq. (6) alignment
+    (PRECEDING) position 0 is not scored: the fallback scores L-2 rows, and a
+    lexical set that starts at position 0 (first_cand) one row fewer.
     """
     d, D, Hq, Hkv = cfg.d, cfg.D, cfg.Hq, cfg.Hkv
+    pre = 1 if PRECEDING else 0
     lex = scan = ver = ver_flops = 0
     for b in range(len(lens)):
         L = int(lens[b])
         T = int(node_count[b])
-        rows = int(cand_count[b]) if int(cand_count[b]) > 0 else max(L - 1, 0)
+        cc = int(cand_count[b])
+        if cc > 0:
+            rows = cc - (1 if pre and first_cand is not None and int(first_cand[b]) == 0 else 0)
+        else:
+            rows = max(L - 1 - pre, 0)
         lex += 4 * L
         scan += 2 * d * rows + 2 * d                                    # scored rows + query
         if T > 0:
@@ -126,7 +135,7 @@ def cpu_baseline(cfg, x, min_seconds=10.0):
         b = done % cfg.B
         oracle.step(x["tokens"], x["lens"], x["bank"], None, cfg.n_max, cfg.k, cfg.W, cfg.S,
                     q_bits=x["q"], kc_bits=x["k_ctx"], vc_bits=x["v_ctx"], kt_bits=x["k_tree"],
-                    vt_bits=x["v_tree"], seqs=[b])
+                    vt_bits=x["v_tree"], seqs=[b], preceding=PRECEDING)
         done += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds and done >= min(cfg.B, 4):
@@ -279,10 +288,11 @@ def measure_embed(adapld, cfg, bufs, s, tokens, lens, x, steps, stream):
         return e0.elapsed_time(e1) / n * 1e3, out
 
     def hidden():
-        return adapld.semantic_topk(s["bank"], lens, bufs.cand_pos, bufs.cand_count, cfg.k)
+        return adapld.semantic_topk(s["bank"], lens, bufs.cand_pos, bufs.cand_count, cfg.k, preceding=PRECEDING)
 
     def embed():
-        return adapld.semantic_topk_embed(s["bank"], tokens, lens, bufs.cand_pos, bufs.cand_count, emb, cfg.k, tau)
+        return adapld.semantic_topk_embed(s["bank"], tokens, lens, bufs.cand_pos, bufs.cand_count, emb, cfg.k, tau,
+                                          preceding=PRECEDING)
 
     adapld.lexical_match(tokens, lens, cfg.n_max, cand_pos=bufs.cand_pos, cand_count=bufs.cand_count,
                          match_n=bufs.match_n)
@@ -468,7 +478,8 @@ def measure(adapld, cfg, name, make_inputs, args):
         s = sets[i % n_copies]
         adapld.lexical_match(tokens, lens, cfg.n_max, cand_pos=bufs.cand_pos, cand_count=bufs.cand_count,
                              match_n=bufs.match_n)
-        adapld.semantic_topk(s["bank"], lens, bufs.cand_pos, bufs.cand_count, cfg.k, topk_pos=bufs.topk_pos,
+        adapld.semantic_topk(s["bank"], lens, bufs.cand_pos, bufs.cand_count, cfg.k, preceding=PRECEDING,
+                             topk_pos=bufs.topk_pos,
                              topk_score=bufs.topk_score, topk_count=bufs.topk_count, kind=bufs.kind,
                              ws=bufs.ws_sem)
         adapld.build_draft_tree(tokens, lens, bufs.topk_pos, bufs.topk_count, bufs.kind, cfg.W, cfg.S,
@@ -488,6 +499,7 @@ def measure(adapld, cfg, name, make_inputs, args):
         run(i)
     torch.cuda.synchronize()
     cand_count = bufs.cand_count.cpu().numpy()
+    first_cand = bufs.cand_pos[:, 0].cpu().numpy()
     node_count = bufs.node_count.cpu().numpy()
     node_depth = bufs.node_depth.cpu().numpy()
     kinds = bufs.kind.cpu().numpy()
@@ -497,7 +509,7 @@ def measure(adapld, cfg, name, make_inputs, args):
     # synchronisation and one event on each side.
     calls = [adapld.StepCall(tokens, lens, sets[j]["bank"], sets[j]["q"], sets[j]["k_ctx"], sets[j]["v_ctx"],
                              sets[j]["k_tree"], sets[j]["v_tree"], n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S,
-                             buffers=bufs, stream=stream) for j in range(n_copies)]
+                             preceding=PRECEDING, buffers=bufs, stream=stream) for j in range(n_copies)]
     for i in range(warmup):
         calls[i % n_copies]()
     # Clocks settle only after some time under load: keep stepping until at
@@ -580,7 +592,7 @@ def measure(adapld, cfg, name, make_inputs, args):
         emb = measure_embed(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
         ptree = measure_paper_tree(adapld, cfg, bufs, sets[0], tokens, lens, x, steps, stream)
 
-    work = algorithmic_work(cfg, x["lens"], cand_count, node_count, node_depth)
+    work = algorithmic_work(cfg, x["lens"], cand_count, node_count, node_depth, first_cand)
     total_b, ver_b = work["total"], work["verify"]
     step_gbs = total_b / (step_ms * 1e-3) / 1e9
     ver_gbs = ver_b / (ver_ms * 1e-3) / 1e9
@@ -606,6 +618,7 @@ def measure(adapld, cfg, name, make_inputs, args):
         "data": "synthetic",
         "config": {"workload": name, "B": cfg.B, "L": cfg.L, "d": cfg.d, "Hq": cfg.Hq, "Hkv": cfg.Hkv,
                    "D": cfg.D, "n_max": cfg.n_max, "k": cfg.k, "W": cfg.W, "S": cfg.S, "T_max": cfg.T_max,
+                   "rerank": "Eq. (6): rows j-1 against row L-2" if PRECEDING else "rows j against row L-1",
                    "input_copies": n_copies},
         "step_hbm": {"algorithmic_bytes": total_b, "achieved_GBs": step_gbs, "peak_GBs": HBM_PEAK_GBS,
                      "frac": step_gbs / HBM_PEAK_GBS},

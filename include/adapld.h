@@ -154,15 +154,22 @@ int adapld_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int 
  * adapld_semantic_topk -- the lexical/semantic backoff rule (Sec. 3.3) and
  * hidden-state reranking (Sec. 3.4).
  *
- * Score s(r) = cos(bank[b, r], q_b) computed with fp32 accumulation (0 when
- * either norm is 0), where q_b = query[b] or, if `query` is NULL, the bank
- * row lens[b]-1.  If cand_count[b] > 0 (lexical hit) the scored rows are
- * cand_pos[b, 0..cand_count[b]-1] and kind = LEX.  Otherwise (lexical miss)
- * every row r in [0, L-2] is scored (the semantic fallback), entries with
- * s < tau are dropped unless tau is NaN (disabled), and kind = SEM if any
- * entry remains, else NONE.  Rows are ranked by score descending, then
- * position ascending, and the first min(k, #rows) are returned.  Candidate
- * positions outside [0, L-1] are skipped.
+ * The score of a candidate position r is computed with fp32 accumulation (0
+ * when either norm is 0):
+ *   preceding = 1  Eq. (6) as printed: the state before the candidate against
+ *                  the state before the anchor, s(r) = cos(bank[b, r-1], q_b),
+ *                  q_b = query[b] or, if `query` is NULL, the bank row
+ *                  lens[b]-2; position 0 has no earlier state and is skipped;
+ *   preceding = 0  s(r) = cos(bank[b, r], q_b), q_b = query[b] or the bank
+ *                  row lens[b]-1.
+ * If cand_count[b] > 0 (lexical hit) the candidates are
+ * cand_pos[b, 0..cand_count[b]-1] and kind = LEX (also when none of them can
+ * be scored).  Otherwise (lexical miss) every position r in [0, L-2] is a
+ * candidate (the semantic fallback), entries with s < tau are dropped unless
+ * tau is NaN (disabled), and kind = SEM if any entry remains, else NONE.
+ * Candidates are ranked by score descending, then position ascending, and
+ * the first min(k, #scored) are returned.  Candidate positions outside
+ * [preceding, L-1] are skipped.
  *
  *   bank       bf16  [B, L_stride, d]       hidden states (row = position)
  *   query      bf16  [B, d] or NULL
@@ -170,19 +177,21 @@ int adapld_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int 
  *   d          8..ADAPLD_MAX_HIDDEN, multiple of 8
  *   k          1..ADAPLD_MAX_K
  *   tau        fallback threshold; NaN disables it
+ *   preceding  0 or 1 (the score alignment above)
  *   topk_pos   int32 [B, k]       (out)     ranked positions
  *   topk_score fp32  [B, k]       (out)     their scores
  *   topk_count int32 [B]          (out)     entries written
  *   kind       int32 [B]          (out)     ADAPLD_KIND_*
  *   ws         workspace of adapld_workspace_bytes(ADAPLD_OP_SEMANTIC_TOPK, B, L_stride, d, k, ...)
  *
- * Errors: NULL_ARG; INVALID_ARG for bad sizes or misaligned bf16 pointers;
- * UNSUPPORTED for d or k beyond the limits, B > ADAPLD_MAX_SEMANTIC_BATCH or
- * B * L_stride > INT32_MAX; WORKSPACE_TOO_SMALL.
+ * Errors: NULL_ARG; INVALID_ARG for bad sizes, preceding outside {0, 1} or
+ * misaligned bf16 pointers; UNSUPPORTED for d or k beyond the limits,
+ * B > ADAPLD_MAX_SEMANTIC_BATCH or B * L_stride > INT32_MAX;
+ * WORKSPACE_TOO_SMALL.
  */
 int adapld_semantic_topk(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
                          const int32_t* cand_pos, const int32_t* cand_count, int B, int L_stride,
-                         int d, int k, float tau, int32_t* topk_pos, float* topk_score,
+                         int d, int k, float tau, int preceding, int32_t* topk_pos, float* topk_score,
                          int32_t* topk_count, int32_t* kind, void* ws, size_t ws_bytes,
                          hipStream_t stream);
 
@@ -227,7 +236,7 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
  * adapld_build_draft_tree and adapld_tree_verify_attn enqueued on `stream`
  * in that order, with no host synchronisation.  Every argument has the
  * meaning, layout and limits it has in those four calls (n_max for the
- * lexical match; d, k, tau and query for the rerank; W, S and T_max for the
+ * lexical match; d, k, tau, preceding and query for the rerank; W, S and T_max for the
  * tree; Hq, Hkv, D and scale for the verify; T_max is also the verify's).
  * All four argument sets are validated before anything is enqueued; the
  * status is that of the first failing check, or of the first failing launch.
@@ -241,7 +250,7 @@ int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const in
 int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank, const uint16_t* query,
                 const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx, const uint16_t* k_tree,
                 const uint16_t* v_tree, int B, int L_stride, int d, int n_max, int k, int W, int S,
-                int T_max, int Hq, int Hkv, int D, float tau, float scale, int32_t* cand_pos,
+                int T_max, int Hq, int Hkv, int D, float tau, int preceding, float scale, int32_t* cand_pos,
                 int32_t* cand_count, int32_t* match_n, int32_t* topk_pos, float* topk_score,
                 int32_t* topk_count, int32_t* kind, int32_t* node_token, int32_t* node_parent,
                 int32_t* node_depth, int32_t* node_src, int32_t* node_count, uint64_t* tree_mask,
@@ -276,7 +285,7 @@ int adapld_step_noalloc(const int32_t* tokens, const int32_t* lens, const uint16
                         const uint16_t* query, const uint16_t* q, const uint16_t* k_ctx,
                         const uint16_t* v_ctx, const uint16_t* k_tree, const uint16_t* v_tree, int B,
                         int L_stride, int d, int n_max, int k, int W, int S, int T_max, int Hq,
-                        int Hkv, int D, float tau, float scale, int32_t* cand_pos,
+                        int Hkv, int D, float tau, int preceding, float scale, int32_t* cand_pos,
                         int32_t* cand_count, int32_t* match_n, int32_t* topk_pos, float* topk_score,
                         int32_t* topk_count, int32_t* kind, int32_t* node_token,
                         int32_t* node_parent, int32_t* node_depth, int32_t* node_src,
@@ -394,10 +403,10 @@ int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint
  * token embedding has cosine >= tau with the embedding of the last token
  * (emb rows of tokens[b, j] and tokens[b, L-1]; a token id outside [0, V)
  * has a zero embedding, cosine 0), in ascending order.  The candidates are
- * then ranked by cos(bank[b, r], q) exactly as adapld_semantic_topk ranks a
- * lexical set, and the first min(k, #candidates) are kept.
- *   bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, topk_*:
- *              as for adapld_semantic_topk (query NULL: bank row L-1)
+ * then ranked exactly as adapld_semantic_topk ranks a lexical set (with the
+ * same `preceding` alignment), and the first min(k, #scored) are kept.
+ *   bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, preceding,
+ *   topk_*:    as for adapld_semantic_topk
  *   tokens     int32 [B, L_stride], the context
  *   emb        bf16 [V, d], the target model's token embeddings
  *              (16-byte aligned; same d as the bank)
@@ -408,14 +417,15 @@ int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint
  *   ws         adapld_workspace_bytes(ADAPLD_OP_SEMANTIC_TOPK_EMBED, B,
  *              L_stride, d, k, ...) bytes, 16-byte aligned
  * Errors: NULL_ARG; INVALID_ARG (B < 0, L_stride < 1, d < 8 or d % 8, k < 1,
- * V < 1, tau not finite, misaligned pointers); UNSUPPORTED (d > 8192,
- * k > 64, B > ADAPLD_MAX_SEMANTIC_BATCH); WORKSPACE_TOO_SMALL.
+ * V < 1, tau not finite, preceding outside {0, 1}, misaligned pointers);
+ * UNSUPPORTED (d > 8192, k > 64, B > ADAPLD_MAX_SEMANTIC_BATCH);
+ * WORKSPACE_TOO_SMALL.
  */
 int adapld_semantic_topk_embed(const uint16_t* bank, const uint16_t* query, const int32_t* tokens,
                                const int32_t* lens, const int32_t* cand_pos, const int32_t* cand_count,
                                const uint16_t* emb, int V, int B, int L_stride, int d, int k, float tau,
-                               int32_t* topk_pos, float* topk_score, int32_t* topk_count, int32_t* kind,
-                               void* ws, size_t ws_bytes, hipStream_t stream);
+                               int preceding, int32_t* topk_pos, float* topk_score, int32_t* topk_count,
+                               int32_t* kind, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Incremental n-gram index -- the lexical anchoring of adapld_lexical_match

@@ -51,19 +51,21 @@ SIGNATURES = {
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "adapld_semantic_topk": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_int,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "adapld_semantic_topk_embed": (ctypes.c_int, [ctypes.c_void_p] * 7 + [ctypes.c_int] * 5 + [ctypes.c_float]
-                                   + [ctypes.c_void_p] * 5 + [ctypes.c_size_t, ctypes.c_void_p]),
+                                   + [ctypes.c_int] + [ctypes.c_void_p] * 5 + [ctypes.c_size_t, ctypes.c_void_p]),
     "adapld_build_draft_tree": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p]),
-    "adapld_step": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 11 + [ctypes.c_float] * 2
+    "adapld_step": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 11
+                    + [ctypes.c_float, ctypes.c_int, ctypes.c_float]
                     + [ctypes.c_void_p] * 16 + [ctypes.c_size_t, ctypes.c_void_p]),
-    "adapld_step_noalloc": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 11 + [ctypes.c_float] * 2
+    "adapld_step_noalloc": (ctypes.c_int, [ctypes.c_void_p] * 9 + [ctypes.c_int] * 11
+                            + [ctypes.c_float, ctypes.c_int, ctypes.c_float]
                             + [ctypes.c_void_p] * 15 + [ctypes.c_void_p]),
     "adapld_build_draft_tree_paper": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int] + [ctypes.c_void_p] * 3
                                       + [ctypes.c_int] + [ctypes.c_void_p] + [ctypes.c_int] * 3
@@ -171,9 +173,11 @@ def lexical_match(tokens, lens, n_max, *, cand_pos=None, cand_count=None, match_
     return cand_pos, cand_count, match_n
 
 
-def semantic_topk(bank, lens, cand_pos, cand_count, k, *, tau=None, query=None, topk_pos=None,
+def semantic_topk(bank, lens, cand_pos, cand_count, k, *, tau=None, query=None, preceding=False, topk_pos=None,
                   topk_score=None, topk_count=None, kind=None, ws=None, stream=None):
-    """Backoff + cosine reranking; returns (topk_pos, topk_score, topk_count, kind)."""
+    """Backoff + cosine reranking; returns (topk_pos, topk_score, topk_count, kind).
+    preceding=True scores each candidate by the state before it against the
+    state before the anchor (Eq. (6) as printed)."""
     lib = load_library()
     B, L_stride, d = bank.shape
     dev = bank.device
@@ -188,7 +192,7 @@ def semantic_topk(bank, lens, cand_pos, cand_count, k, *, tau=None, query=None, 
         _ptr(bank, "bank", _BF16_DTYPES), _ptr(query, "query", _BF16_DTYPES, (B, d), nullable=True),
         _ptr(lens, "lens", (torch.int32,), (B,)), _ptr(cand_pos, "cand_pos", (torch.int32,), (B, L_stride)),
         _ptr(cand_count, "cand_count", (torch.int32,), (B,)), B, L_stride, d, k,
-        float("nan") if tau is None else float(tau),
+        float("nan") if tau is None else float(tau), int(bool(preceding)),
         _ptr(topk_pos, "topk_pos", (torch.int32,), (B, k)), _ptr(topk_score, "topk_score", (torch.float32,), (B, k)),
         _ptr(topk_count, "topk_count", (torch.int32,), (B,)), _ptr(kind, "kind", (torch.int32,), (B,)),
         _ptr(ws, "ws", (torch.uint8,)), ws.numel(), _stream(stream))
@@ -196,8 +200,8 @@ def semantic_topk(bank, lens, cand_pos, cand_count, k, *, tau=None, query=None, 
     return topk_pos, topk_score, topk_count, kind
 
 
-def semantic_topk_embed(bank, tokens, lens, cand_pos, cand_count, emb, k, tau, *, query=None, topk_pos=None,
-                        topk_score=None, topk_count=None, kind=None, ws=None, stream=None):
+def semantic_topk_embed(bank, tokens, lens, cand_pos, cand_count, emb, k, tau, *, query=None, preceding=False,
+                        topk_pos=None, topk_score=None, topk_count=None, kind=None, ws=None, stream=None):
     """Backoff with the token-embedding fallback, then the hidden-state
     rerank; returns (topk_pos, topk_score, topk_count, kind)."""
     lib = load_library()
@@ -215,7 +219,7 @@ def semantic_topk_embed(bank, tokens, lens, cand_pos, cand_count, emb, k, tau, *
         _ptr(bank, "bank", _BF16_DTYPES), _ptr(query, "query", _BF16_DTYPES, (B, d), nullable=True),
         _ptr(tokens, "tokens", (torch.int32,), (B, L_stride)), _ptr(lens, "lens", (torch.int32,), (B,)),
         _ptr(cand_pos, "cand_pos", (torch.int32,), (B, L_stride)), _ptr(cand_count, "cand_count", (torch.int32,), (B,)),
-        _ptr(emb, "emb", _BF16_DTYPES, (V, d)), V, B, L_stride, d, k, float(tau),
+        _ptr(emb, "emb", _BF16_DTYPES, (V, d)), V, B, L_stride, d, k, float(tau), int(bool(preceding)),
         _ptr(topk_pos, "topk_pos", (torch.int32,), (B, k)), _ptr(topk_score, "topk_score", (torch.float32,), (B, k)),
         _ptr(topk_count, "topk_count", (torch.int32,), (B,)), _ptr(kind, "kind", (torch.int32,), (B,)),
         _ptr(ws, "ws", (torch.uint8,)), ws.numel(), _stream(stream))
@@ -465,7 +469,8 @@ class StepCall:
     The stream is the one given, else the current stream at construction."""
 
     def __init__(self, tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None,
-                 query=None, scale=None, buffers: StepBuffers | None = None, stream=None, noalloc=False):
+                 query=None, preceding=False, scale=None, buffers: StepBuffers | None = None, stream=None,
+                 noalloc=False):
         B, L_stride = tokens.shape
         _, _, d = bank.shape
         _, T_max, Hq, D = q.shape
@@ -488,7 +493,7 @@ class StepCall:
             _ptr(q, "q", bf16), _ptr(k_ctx, "k_ctx", bf16, (B, Hkv, L_stride, D)),
             _ptr(v_ctx, "v_ctx", bf16, (B, Hkv, L_stride, D)), _ptr(k_tree, "k_tree", bf16, (B, T_max, Hkv, D)),
             _ptr(v_tree, "v_tree", bf16, (B, T_max, Hkv, D)),
-            B, L_stride, d, n_max, k, W, S, T_max, Hq, Hkv, D, tau, scale,
+            B, L_stride, d, n_max, k, W, S, T_max, Hq, Hkv, D, tau, int(bool(preceding)), scale,
             _ptr(bf.cand_pos, "cand_pos", i32, (B, L_stride)), _ptr(bf.cand_count, "cand_count", i32, (B,)),
             _ptr(bf.match_n, "match_n", i32, (B,)), _ptr(bf.topk_pos, "topk_pos", i32, (B, k)),
             _ptr(bf.topk_score, "topk_score", (torch.float32,), (B, k)),
@@ -510,7 +515,7 @@ class StepCall:
 
 
 def step(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None, query=None,
-         scale=None, buffers: StepBuffers | None = None, stream=None, noalloc=False):
+         preceding=False, scale=None, buffers: StepBuffers | None = None, stream=None, noalloc=False):
     """One draft-and-verify step: adapld_step, i.e. the four entry points
     back to back on one stream from one native call (adapld_step_noalloc
     with noalloc=True: the library's own device workspace, nothing allocated
@@ -520,11 +525,12 @@ def step(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S,
     is taken on the device.  Returns the StepBuffers holding every output.
     """
     return StepCall(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, n_max=n_max, k=k, W=W, S=S, tau=tau,
-                    query=query, scale=scale, buffers=buffers, stream=stream, noalloc=noalloc)()
+                    query=query, preceding=preceding, scale=scale, buffers=buffers, stream=stream,
+                    noalloc=noalloc)()
 
 
 def step_calls(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k, W, S, tau=None, query=None,
-               scale=None, buffers: StepBuffers | None = None, stream=None):
+               preceding=False, scale=None, buffers: StepBuffers | None = None, stream=None):
     """The same step as four separate entry-point calls (the route a caller
     takes to put its own work or events between them)."""
     B, L_stride = tokens.shape
@@ -535,7 +541,8 @@ def step_calls(tokens, lens, bank, q, k_ctx, v_ctx, k_tree, v_tree, *, n_max, k,
     bf = buffers
     lexical_match(tokens, lens, n_max, cand_pos=bf.cand_pos, cand_count=bf.cand_count, match_n=bf.match_n,
                   stream=stream)
-    semantic_topk(bank, lens, bf.cand_pos, bf.cand_count, k, tau=tau, query=query, topk_pos=bf.topk_pos,
+    semantic_topk(bank, lens, bf.cand_pos, bf.cand_count, k, tau=tau, query=query, preceding=preceding,
+                  topk_pos=bf.topk_pos,
                   topk_score=bf.topk_score, topk_count=bf.topk_count, kind=bf.kind, ws=bf.ws_sem, stream=stream)
     build_draft_tree(tokens, lens, bf.topk_pos, bf.topk_count, bf.kind, W, S, T_max, node_token=bf.node_token,
                      node_parent=bf.node_parent, node_depth=bf.node_depth, node_src=bf.node_src,

@@ -9,7 +9,7 @@ namespace {
 
 thread_local int g_last_hip_error = 0;
 
-constexpr int kVersion = 10400;  // 1.4.0: the incremental n-gram index
+constexpr int kVersion = 20000;  // 2.0.0: the rerank takes the score alignment (preceding)
 
 bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
@@ -182,30 +182,32 @@ int adapld_lexical_match(const int32_t* tokens, const int32_t* lens, int B, int 
 
 int adapld_semantic_topk(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
                          const int32_t* cand_pos, const int32_t* cand_count, int B, int L_stride,
-                         int d, int k, float tau, int32_t* topk_pos, float* topk_score,
+                         int d, int k, float tau, int preceding, int32_t* topk_pos, float* topk_score,
                          int32_t* topk_count, int32_t* kind, void* ws, size_t ws_bytes,
                          hipStream_t stream) {
   if (const int st = check_semantic(bank, query, lens, cand_pos, cand_count, B, L_stride, d, k,
                                     tau, topk_pos, topk_score, topk_count, kind, ws, ws_bytes);
       st != ADAPLD_OK || B == 0)
     return st;
+  if (preceding != 0 && preceding != 1) return ADAPLD_ERR_INVALID_ARG;
   return hip_status(adapld::launch_semantic_topk(bank, query, lens, cand_pos, cand_count, B,
                                                  L_stride, d, k, tau, topk_pos, topk_score,
                                                  topk_count, kind, static_cast<uint64_t*>(ws),
-                                                 nullptr, 0, stream));
+                                                 nullptr, 0, stream, 1, nullptr, preceding));
 }
 
 int adapld_semantic_topk_embed(const uint16_t* bank, const uint16_t* query, const int32_t* tokens,
                                const int32_t* lens, const int32_t* cand_pos, const int32_t* cand_count,
                                const uint16_t* emb, int V, int B, int L_stride, int d, int k, float tau,
-                               int32_t* topk_pos, float* topk_score, int32_t* topk_count, int32_t* kind,
-                               void* ws, size_t ws_bytes, hipStream_t stream) {
+                               int preceding, int32_t* topk_pos, float* topk_score, int32_t* topk_count,
+                               int32_t* kind, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (B < 0) return ADAPLD_ERR_INVALID_ARG;
   if (B == 0) return ADAPLD_OK;
   if (!bank || !tokens || !lens || !cand_pos || !cand_count || !emb || !topk_pos || !topk_score ||
       !topk_count || !kind || !ws)
     return ADAPLD_ERR_NULL_ARG;
-  if (L_stride < 1 || d < 8 || d % 8 != 0 || k < 1 || V < 1 || !std::isfinite(tau))
+  if (L_stride < 1 || d < 8 || d % 8 != 0 || k < 1 || V < 1 || !std::isfinite(tau) ||
+      (preceding != 0 && preceding != 1))
     return ADAPLD_ERR_INVALID_ARG;
   if (d > ADAPLD_MAX_HIDDEN || k > ADAPLD_MAX_K || B > ADAPLD_MAX_SEMANTIC_BATCH ||
       (int64_t)B * L_stride > INT32_MAX)
@@ -221,7 +223,7 @@ int adapld_semantic_topk_embed(const uint16_t* bank, const uint16_t* query, cons
   uint64_t* keys = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + head);
   return hip_status(adapld::launch_semantic_topk(bank, query, lens, cands, counts, B, L_stride, d, k, NAN,
                                                  topk_pos, topk_score, topk_count, kind, keys, kinds, 1,
-                                                 stream));
+                                                 stream, 1, nullptr, preceding));
 }
 
 int adapld_build_draft_tree(const int32_t* tokens, const int32_t* lens, const int32_t* topk_pos,
@@ -288,13 +290,14 @@ int adapld_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, const uint
 int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank, const uint16_t* query,
                 const uint16_t* q, const uint16_t* k_ctx, const uint16_t* v_ctx, const uint16_t* k_tree,
                 const uint16_t* v_tree, int B, int L_stride, int d, int n_max, int k, int W, int S,
-                int T_max, int Hq, int Hkv, int D, float tau, float scale, int32_t* cand_pos,
+                int T_max, int Hq, int Hkv, int D, float tau, int preceding, float scale, int32_t* cand_pos,
                 int32_t* cand_count, int32_t* match_n, int32_t* topk_pos, float* topk_score,
                 int32_t* topk_count, int32_t* kind, int32_t* node_token, int32_t* node_parent,
                 int32_t* node_depth, int32_t* node_src, int32_t* node_count, uint64_t* tree_mask,
                 uint16_t* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (B < 0) return ADAPLD_ERR_INVALID_ARG;
   if (B == 0) return ADAPLD_OK;
+  if (preceding != 0 && preceding != 1) return ADAPLD_ERR_INVALID_ARG;
   if (!ws) return ADAPLD_ERR_NULL_ARG;
   if (misaligned16(ws)) return ADAPLD_ERR_INVALID_ARG;
   if (k < 1 || L_stride < 1) return ADAPLD_ERR_INVALID_ARG;
@@ -324,7 +327,7 @@ int adapld_step(const int32_t* tokens, const int32_t* lens, const uint16_t* bank
   if (e == hipSuccess)
     e = adapld::launch_semantic_topk(bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, tau,
                                      topk_pos, topk_score, topk_count, kind, static_cast<uint64_t*>(ws),
-                                     nullptr, 0, stream, 1, &tree);
+                                     nullptr, 0, stream, 1, &tree, preceding);
   if (e == hipSuccess)
     e = adapld::launch_tree_verify_attn(q, k_ctx, v_ctx, k_tree, v_tree, lens, node_count, tree_mask, B,
                                         L_stride, T_max, Hq, Hkv, scale, out, lse, ws_ver,

@@ -85,13 +85,16 @@ struct TreeOut {
 };
 
 // With `tree`, the merge kernel also builds each sequence's draft tree from
-// the ranked list it has just formed (the step's fused rank + tree).
+// the ranked list it has just formed (the step's fused rank + tree).  With
+// `preceding`, position j is scored by bank row j-1 (Eq. (6)); the rerank
+// lists of the paper's construction already hold the rows t-1 and pass 0.
 hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, const int32_t* lens,
                                 const int32_t* cand_pos, const int32_t* cand_count, int B,
                                 int L_stride, int d, int k, float tau, int32_t* topk_pos,
                                 float* topk_score, int32_t* topk_count, int32_t* kind,
                                 uint64_t* ws_keys, const int32_t* cand_kind, int rerank_only,
-                                hipStream_t stream, int seq_div = 1, const TreeOut* tree = nullptr);
+                                hipStream_t stream, int seq_div = 1, const TreeOut* tree = nullptr,
+                                int preceding = 0);
 
 hipError_t launch_build_draft_tree(const int32_t* tokens, const int32_t* lens,
                                    const int32_t* topk_pos, const int32_t* topk_count,

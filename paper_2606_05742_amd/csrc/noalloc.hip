@@ -49,7 +49,7 @@ extern "C" int adapld_step_noalloc(
     const int32_t* tokens, const int32_t* lens, const uint16_t* bank, const uint16_t* query, const uint16_t* q,
     const uint16_t* k_ctx, const uint16_t* v_ctx, const uint16_t* k_tree, const uint16_t* v_tree, int B,
     int L_stride, int d, int n_max, int k, int W, int S, int T_max, int Hq, int Hkv, int D, float tau,
-    float scale, int32_t* cand_pos, int32_t* cand_count, int32_t* match_n, int32_t* topk_pos,
+    int preceding, float scale, int32_t* cand_pos, int32_t* cand_count, int32_t* match_n, int32_t* topk_pos,
     float* topk_score, int32_t* topk_count, int32_t* kind, int32_t* node_token, int32_t* node_parent,
     int32_t* node_depth, int32_t* node_src, int32_t* node_count, uint64_t* tree_mask, uint16_t* out,
     float* lse, hipStream_t stream) {
@@ -63,7 +63,7 @@ extern "C" int adapld_step_noalloc(
   const hipError_t e = scratch_on_current_device(&ws);
   if (e != hipSuccess) return adapld::record_hip_error(e);
   return adapld_step(tokens, lens, bank, query, q, k_ctx, v_ctx, k_tree, v_tree, B, L_stride, d, n_max, k, W,
-                     S, T_max, Hq, Hkv, D, tau, scale, cand_pos, cand_count, match_n, topk_pos, topk_score,
+                     S, T_max, Hq, Hkv, D, tau, preceding, scale, cand_pos, cand_count, match_n, topk_pos, topk_score,
                      topk_count, kind, node_token, node_parent, node_depth, node_src, node_count, tree_mask,
                      out, lse, ws, kScratchBytes, stream);
 }

@@ -54,6 +54,8 @@ struct ScanArgs {
   const int32_t* cand_kind;       // kind of a non-empty candidate set (NULL: LEX)
   int rerank_only;                // 1: an empty candidate set scores nothing (kind NONE)
   int seq_div;                    // list s reads the bank rows and query of sequence s / seq_div
+  int pre;                        // 1: position j is scored by bank row j-1 and the default query
+                                  // is row L-2 (Eq. (6)); position 0 is not scored
 };
 
 __device__ __forceinline__ void seq_rows(const ScanArgs& a, int b, int& L, int& cc, int& nrows) {
@@ -174,7 +176,7 @@ __global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const Sc
       const int b = seq_of(gl);
       const int i = gl - s_start[b];
       const int rr = s_cc[b] > 0 ? a.cand_pos[(size_t)b * a.L_stride + i] : i;
-      r = rr >= 0 && rr < s_len[b] ? rr : -1;   // rows outside [0, L) are skipped
+      r = rr >= a.pre && rr < s_len[b] ? rr : -1;   // positions outside [pre, L) are skipped
     }
     s_win[wave][lane] = r;
   };
@@ -190,7 +192,7 @@ __global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const Sc
     if (lane == 0) s_pos[wave][slot] = r;
     // A skipped row still loads (row 0 of its sequence) so that every row
     // counts NIT loads in vmcnt.
-    const uint16_t* row = a.bank + ((size_t)(pb / a.seq_div) * a.L_stride + (r >= 0 ? r : 0)) * d;
+    const uint16_t* row = a.bank + ((size_t)(pb / a.seq_div) * a.L_stride + (r >= 0 ? r - a.pre : 0)) * d;
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the slot's previous row has been read
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
@@ -210,7 +212,7 @@ __global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const Sc
   };
   auto query_of = [&](int b) {
     return a.query ? a.query + (size_t)(b / a.seq_div) * d
-                   : a.bank + ((size_t)(b / a.seq_div) * a.L_stride + max(s_len[b] - 1, 0)) * d;
+                   : a.bank + ((size_t)(b / a.seq_div) * a.L_stride + max(s_len[b] - 1 - a.pre, 0)) * d;
   };
   auto begin_segment = [&](int g) {
     flush();
@@ -447,9 +449,9 @@ hipError_t launch_semantic_topk(const uint16_t* bank, const uint16_t* query, con
                                 int L_stride, int d, int k, float tau, int32_t* topk_pos,
                                 float* topk_score, int32_t* topk_count, int32_t* kind,
                                 uint64_t* ws_keys, const int32_t* cand_kind, int rerank_only,
-                                hipStream_t stream, int seq_div, const TreeOut* tree) {
+                                hipStream_t stream, int seq_div, const TreeOut* tree, int preceding) {
   ScanArgs a{bank, query, lens, cand_pos, cand_count, B, L_stride, d, k, scan_lists(L_stride), ws_keys,
-             cand_kind, rerank_only, seq_div};
+             cand_kind, rerank_only, seq_div, preceding ? 1 : 0};
   const int nit = (d + 8 * kWave - 1) / (8 * kWave);
   switch (nit) {
 #define ADAPLD_SCAN_CASE(n) \

@@ -54,19 +54,21 @@ def near_tie(a, b):
     return abs(a - b) <= TIE_RTOL * max(abs(a), abs(b)) + TIE_ATOL
 
 
-def check_ranked(bank, query, cand, k, tau, g_kind, g_pos, g_score, ctx=""):
-    """Compare one sequence's GPU ranked list with the oracle; returns the oracle's record."""
-    o_kind, o_pos, o_score = oracle.semantic_topk(bank, query, cand, k, tau)
+def check_ranked(bank, query, cand, k, tau, g_kind, g_pos, g_score, ctx="", preceding=False):
+    """Compare one sequence's GPU ranked list with the oracle; returns the oracle's record.
+    preceding: the alignment of Eq. (6) as printed (position j scored by row j-1)."""
+    o_kind, o_pos, o_score = oracle.semantic_topk(bank, query, cand, k, tau, preceding=preceding)
     assert g_kind == o_kind, f"{ctx}: kind {g_kind} != {o_kind}"
     L = bank.shape[0]
-    q = bank[L - 1] if query is None else query
+    sh = 1 if preceding else 0
+    q = (bank[L - 1 - sh] if L - 1 - sh >= 0 else np.zeros(bank.shape[1])) if query is None else query
     if g_pos == o_pos:
         np.testing.assert_allclose(g_score, o_score, rtol=0, atol=SCORE_ATOL, err_msg=ctx)
         return o_kind, o_pos, o_score
     # Positions differ: every difference must be explained by near-ties.
-    sig = list(oracle.cosine_rows(bank, g_pos, q)) if g_pos else []
+    sig = list(oracle.cosine_rows(bank, [p - sh for p in g_pos], q)) if g_pos else []
     np.testing.assert_allclose(g_score, sig, rtol=0, atol=SCORE_ATOL, err_msg=ctx)
-    pool = set(cand) if len(cand) > 0 else set(range(L - 1))
+    pool = {c for c in cand if c >= sh} if len(cand) > 0 else set(range(sh, L - 1))
     assert set(g_pos) <= pool and len(set(g_pos)) == len(g_pos), ctx
     for i in range(len(sig)):
         for j in range(i + 1, len(sig)):

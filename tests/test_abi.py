@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(lib):
 def test_status_strings(lib):
     for code in (OK, NULL, INVALID, UNSUPPORTED, WS_SMALL, -5, 123):
         assert lib.adapld_status_string(code)
-    assert lib.adapld_version() == 10400
+    assert lib.adapld_version() == 20000
     assert lib.adapld_last_hip_error() == 0
 
 
@@ -81,7 +81,7 @@ def test_embed_validation(lib):
     nan = float("nan")
     args = lambda **kw: [kw.get(n, v) for n, v in (  # noqa: E731
         ("bank", P), ("query", N), ("tokens", P), ("lens", P), ("cand_pos", P), ("cand_count", P), ("emb", P),
-        ("V", 100), ("B", 2), ("L_stride", 64), ("d", 128), ("k", 8), ("tau", 0.5),
+        ("V", 100), ("B", 2), ("L_stride", 64), ("d", 128), ("k", 8), ("tau", 0.5), ("pre", 1),
         ("pos", P), ("score", P), ("count", P), ("kind", P), ("ws", P), ("ws_bytes", 1 << 30), ("stream", N))]
     assert f(*args(B=0)) == OK
     assert f(*args(B=-1)) == INVALID
@@ -89,6 +89,7 @@ def test_embed_validation(lib):
     assert f(*args(tokens=N)) == NULL
     assert f(*args(ws=N)) == NULL
     assert f(*args(tau=nan)) == INVALID                 # the threshold is required
+    assert f(*args(pre=2)) == INVALID                   # the alignment is 0 or 1
     assert f(*args(V=0)) == INVALID
     assert f(*args(d=12)) == INVALID
     assert f(*args(k=65)) == UNSUPPORTED
@@ -104,12 +105,13 @@ def test_step_validation(lib):
     args = lambda **kw: [kw.get(n, v) for n, v in (  # noqa: E731
         ("tokens", P), ("lens", P), ("bank", P), ("query", N), ("q", P), ("k_ctx", P), ("v_ctx", P),
         ("k_tree", P), ("v_tree", P), ("B", 2), ("L_stride", 64), ("d", 128), ("n_max", 3), ("k", 8),
-        ("W", 4), ("S", 4), ("T_max", 20), ("Hq", 8), ("Hkv", 2), ("D", 128), ("tau", nan), ("scale", 0.1),
-        *[(f"o{i}", P) for i in range(15)], ("ws", P), ("ws_bytes", 1 << 30), ("stream", N))]
+        ("W", 4), ("S", 4), ("T_max", 20), ("Hq", 8), ("Hkv", 2), ("D", 128), ("tau", nan), ("pre", 1),
+        ("scale", 0.1), *[(f"o{i}", P) for i in range(15)], ("ws", P), ("ws_bytes", 1 << 30), ("stream", N))]
     assert f(*args(B=0)) == OK
     assert f(*args(B=-1)) == INVALID
     assert f(*args(ws=N)) == NULL
     assert f(*args(ws=ctypes.c_void_p(0x10008))) == INVALID
+    assert f(*args(pre=-1)) == INVALID
     assert f(*args(tokens=N)) == NULL                 # the lexical call's check
     assert f(*args(n_max=65)) == UNSUPPORTED
     assert f(*args(d=12)) == INVALID                  # the rerank's
@@ -198,7 +200,7 @@ def test_semantic_validation(lib):
     nan = float("nan")
     args = lambda **kw: [kw.get(n, v) for n, v in [  # noqa: E731
         ("bank", P), ("query", N), ("lens", P), ("cand_pos", P), ("cand_count", P), ("B", 2), ("L", 64),
-        ("d", 256), ("k", 8), ("tau", nan), ("tp", P), ("ts", P), ("tc", P), ("kind", P), ("ws", P),
+        ("d", 256), ("k", 8), ("tau", nan), ("pre", 0), ("tp", P), ("ts", P), ("tc", P), ("kind", P), ("ws", P),
         ("wsb", 1 << 20), ("st", N)]]
     assert f(*args(bank=N)) == NULL
     assert f(*args(ws=N)) == NULL
@@ -209,6 +211,7 @@ def test_semantic_validation(lib):
     assert f(*args(d=8200)) == UNSUPPORTED
     assert f(*args(bank=ctypes.c_void_p(0x10008))) == INVALID      # misaligned bf16 rows
     assert f(*args(wsb=16)) == WS_SMALL
+    assert f(*args(pre=2)) == INVALID                              # the alignment is 0 or 1
     assert f(*args(B=2049)) == UNSUPPORTED                         # sequence offsets live in LDS
     assert f(*args(B=2048, L=1 << 20)) == UNSUPPORTED              # B * L_stride beyond int32
 
@@ -260,8 +263,8 @@ def test_step_noalloc_validation(lib):
     cap = 64 << 20
     args = lambda **kw: [kw.get(n, v) for n, v in (  # noqa: E731
         *((f"p{i}", P) for i in range(9)), ("B", 2), ("L_stride", 64), ("d", 128), ("n_max", 3), ("k", 8),
-        ("W", 4), ("S", 4), ("T_max", 20), ("Hq", 8), ("Hkv", 2), ("D", 128), ("tau", float("nan")), ("scale", 0.1),
-        *((f"o{i}", P) for i in range(15)), ("stream", N))]
+        ("W", 4), ("S", 4), ("T_max", 20), ("Hq", 8), ("Hkv", 2), ("D", 128), ("tau", float("nan")), ("pre", 0),
+        ("scale", 0.1), *((f"o{i}", P) for i in range(15)), ("stream", N))]
     assert f(*args(B=0)) == OK
     assert f(*args(B=-1)) == INVALID
     big = dict(B=2048, L_stride=4096, k=64)   # the rerank's lists alone: 2048 * 1024 * 64 * 8 bytes

@@ -36,14 +36,15 @@ def margin_ok(E, tokens, lens, tau, margin=1e-3):
     return True
 
 
-def run_and_check(cfg, x, E_bits, tau, k, ctx, exact=False):
-    """exact: the table's cosines are exact in fp32 (no margin around tau needed)."""
+def run_and_check(cfg, x, E_bits, tau, k, ctx, exact=False, preceding=False):
+    """exact: the table's cosines are exact in fp32 (no margin around tau needed);
+    preceding: the rerank's alignment (Eq. (6) as printed)."""
     E = oracle.bf16_bits_to_f64(E_bits)
     assert exact or margin_ok(E, x["tokens"], x["lens"], tau), "pick another tau: a cosine sits on it"
     tokens, lens = dev_i32(x["tokens"]), dev_i32(x["lens"])
     cp, cc, mn = adapld.lexical_match(tokens, lens, cfg.n_max)
     pos, sc, cnt, kind = adapld.semantic_topk_embed(dev_bf16(x["bank"]), tokens, lens, cp, cc, dev_bf16(E_bits),
-                                                    k, tau)
+                                                    k, tau, preceding=preceding)
     torch.cuda.synchronize()
     pos, sc, cnt, kind = (t.cpu().numpy() for t in (pos, sc, cnt, kind))
     kinds = []
@@ -59,7 +60,8 @@ def run_and_check(cfg, x, E_bits, tau, k, ctx, exact=False):
             continue
         n = int(cnt[b])
         check_ranked(oracle.bf16_bits_to_f64(x["bank"][b, :L]), None, Cs, k, None, oracle.KIND_LEX,
-                     [int(p) for p in pos[b, :n]], [float(s) for s in sc[b, :n]], f"{ctx} b={b}")
+                     [int(p) for p in pos[b, :n]], [float(s) for s in sc[b, :n]], f"{ctx} b={b}",
+                     preceding=preceding)
     return kinds
 
 
@@ -69,6 +71,15 @@ def test_embedding_fallback(L, d, k, tau):
     x = make_inputs(cfg, with_verify=False)
     E_bits = emb_table(cfg.V + 8, d, clusters=6, seed=L, zero_rows=(7,))   # ids reach V (c.17)
     kinds = run_and_check(cfg, x, E_bits, tau, k, f"L={L}")
+    assert oracle.KIND_SEM in kinds and oracle.KIND_LEX in kinds, kinds
+
+
+def test_embedding_fallback_preceding():
+    """The embedding set ranked with Eq. (6)'s alignment (rows j-1, query row L-2)."""
+    cfg = small_config(B=8, L=700, d=256, k=8, n_max=3, seed=147, V=60, forced_every=2)
+    x = make_inputs(cfg, with_verify=False)
+    E_bits = emb_table(cfg.V + 8, 256, clusters=6, seed=9, zero_rows=(7,))
+    kinds = run_and_check(cfg, x, E_bits, 0.5, 8, "preceding", preceding=True)
     assert oracle.KIND_SEM in kinds and oracle.KIND_LEX in kinds, kinds
 
 

@@ -30,9 +30,10 @@ def upload(x):
                 k_tree=dev_bf16(x["k_tree"]), v_tree=dev_bf16(x["v_tree"]))
 
 
-def run_step(cfg, d, tau=None, query=None):
+def run_step(cfg, d, tau=None, query=None, preceding=False):
     bf = adapld.step(d["tokens"], d["lens"], d["bank"], d["q"], d["k_ctx"], d["v_ctx"], d["k_tree"],
-                     d["v_tree"], n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, tau=tau, query=query)
+                     d["v_tree"], n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, tau=tau, query=query,
+                     preceding=preceding)
     torch.cuda.synchronize()
     g = {}
     for name in ("cand_pos", "cand_count", "match_n", "topk_pos", "topk_score", "topk_count", "kind",
@@ -42,7 +43,7 @@ def run_step(cfg, d, tau=None, query=None):
     return g
 
 
-def check_all(cfg, x, g, tau=None, query_bits=None, verify_nodes=None, seqs=None, ctx=""):
+def check_all(cfg, x, g, tau=None, query_bits=None, verify_nodes=None, seqs=None, ctx="", preceding=False):
     """Compare the GPU step with the oracle; verify_nodes=None checks every node."""
     B = x["tokens"].shape[0]
     seqs = range(B) if seqs is None else seqs
@@ -61,7 +62,8 @@ def check_all(cfg, x, g, tau=None, query_bits=None, verify_nodes=None, seqs=None
         kind = int(g["kind"][b])
         tc = int(g["topk_count"][b])
         gpos = [int(p) for p in g["topk_pos"][b, :tc]]
-        check_ranked(bank, qv, C, cfg.k, tau, kind, gpos, [float(s) for s in g["topk_score"][b, :tc]], c)
+        check_ranked(bank, qv, C, cfg.k, tau, kind, gpos, [float(s) for s in g["topk_score"][b, :tc]], c,
+                     preceding=preceding)
         kinds.append(kind)
         t = check_tree(M, kind, gpos, cfg.W, cfg.S, g, b, c)
         T = t["T"]
@@ -103,6 +105,37 @@ def test_step_small(kw):
     g = run_step(cfg, upload(x))
     kinds = check_all(cfg, x, g, ctx=str(kw))
     log("kinds", kinds)
+
+
+@pytest.mark.parametrize("kw", [SMALL[0], SMALL[1], SMALL[3], SMALL[4]], ids=["small0", "small1", "small3", "small4"])
+def test_step_small_preceding(kw):
+    """Eq. (6) as printed: every candidate scored by the bank row before it
+    against the row before the anchor (the fallback from position 1)."""
+    cfg = small_config(**kw)
+    x = make_inputs(cfg)
+    g = run_step(cfg, upload(x), preceding=True)
+    check_all(cfg, x, g, ctx=f"preceding {kw}", preceding=True)
+
+
+def test_preceding_query_tau_and_position_zero():
+    """The preceding alignment with an explicit query and a threshold, and a
+    lexical set that holds only position 0 (nothing to score: kind LEX, no
+    tree)."""
+    cfg = small_config(B=3, L=600, d=256, Hq=8, Hkv=2, k=8, W=4, S=5, n_max=1, seed=97, forced_every=3)
+    x = make_inputs(cfg)
+    rng = np.random.default_rng(5)
+    qbits = x["bank"][np.arange(cfg.B), rng.integers(0, cfg.L - 1, size=cfg.B)].copy()
+    g = run_step(cfg, upload(x), tau=0.1, query=dev_bf16(qbits), preceding=True)
+    check_all(cfg, x, g, tau=0.1, query_bits=qbits, ctx="preceding query", preceding=True)
+    # sequence 1: the last token occurs only at position 0 of the context
+    b, L = 1, int(x["lens"][1])
+    fresh = int(x["tokens"].max()) + 1
+    x["tokens"][b, 0] = fresh
+    x["tokens"][b, L - 1] = fresh
+    g = run_step(cfg, upload(x), preceding=True)
+    assert int(g["cand_count"][b]) == 1 and int(g["cand_pos"][b, 0]) == 0
+    assert int(g["kind"][b]) == oracle.KIND_LEX and int(g["topk_count"][b]) == 0 and int(g["node_count"][b]) == 0
+    check_all(cfg, x, g, ctx="position 0 only", preceding=True)
 
 
 EDGE = {
@@ -296,16 +329,17 @@ def test_deterministic_repeats():
 
 @pytest.mark.parametrize("name", list(CONFIGS))
 def test_full_config(name):
+    """The five workloads as bench.py runs them (Eq. (6)'s alignment)."""
     cfg = CONFIGS[name]
     log(f"[{name}] generating")
     x = make_inputs(cfg)
     log(f"[{name}] uploading and running")
-    g = run_step(cfg, upload(x))
+    g = run_step(cfg, upload(x), preceding=True)
     log(f"[{name}] comparing")
     nodes = [0, cfg.S, cfg.T_max - 1]
     seqs = sorted(set([0, cfg.B - 1] + [b for b in range(cfg.B) if x["forced"][b]][:2]))
     # lexical and ranking on every sequence, verify on sampled sequences and nodes
-    kinds = check_all(cfg, x, g, verify_nodes=nodes, seqs=seqs, ctx=name)
+    kinds = check_all(cfg, x, g, verify_nodes=nodes, seqs=seqs, ctx=name, preceding=True)
     rest = [b for b in range(cfg.B) if b not in seqs]
     for b in rest:
         L = int(x["lens"][b])
@@ -315,7 +349,7 @@ def test_full_config(name):
         tc = int(g["topk_count"][b])
         gpos = [int(p) for p in g["topk_pos"][b, :tc]]
         check_ranked(LazyBank(x["bank"][b], L), None, C, cfg.k, None, int(g["kind"][b]), gpos,
-                     [float(s) for s in g["topk_score"][b, :tc]], f"{name} b={b}")
+                     [float(s) for s in g["topk_score"][b, :tc]], f"{name} b={b}", preceding=True)
         check_tree(x["tokens"][b, :L], int(g["kind"][b]), gpos, cfg.W, cfg.S, g, b, f"{name} b={b}")
     log(f"[{name}] kinds(sampled)={kinds} fallback={int((g['cand_count'] == 0).sum())}/{cfg.B}")
 
@@ -327,8 +361,8 @@ def test_benchmark_workload_every_node():
     nodes."""
     cfg = CONFIGS["b16_l8192_gqa32x8"]
     x = make_inputs(cfg)
-    g = run_step(cfg, upload(x))
+    g = run_step(cfg, upload(x), preceding=True)
     hit = next(b for b in range(cfg.B) if not x["forced"][b] and int(g["cand_count"][b]) > 0)
     forced = next(b for b in range(cfg.B) if x["forced"][b])
-    check_all(cfg, x, g, verify_nodes=None, seqs=[hit, forced], ctx="every node")
+    check_all(cfg, x, g, verify_nodes=None, seqs=[hit, forced], ctx="every node", preceding=True)
     assert int(g["node_count"][hit]) > 1 and int(g["node_count"][forced]) > 1
