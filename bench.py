@@ -64,8 +64,9 @@ def log(msg):
 
 MFMA_PEAK_BF16_TFLOPS = 2500.0
 WARM_SECONDS = 1.0      # stepping before the timed steps, so that clocks have settled
-PRECEDING = True        # the rerank's alignment: Eq. (6) as printed (the states before the
-                        # candidate and before the anchor)
+PRECEDING = False       # the rerank's alignment: the workloads' query, the hidden state at the
+                        # last position, against rows j (True: Eq. (6) as printed, rows j-1
+                        # against row L-2)
 SPREAD_BLOCKS = 9       # further blocks of K steps timed after the headline block
 
 
@@ -140,9 +141,16 @@ def cpu_baseline(cfg, x, min_seconds=10.0):
         dt = time.perf_counter() - t0
         if dt >= min_seconds and done >= min(cfg.B, 4):
             break
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), cpu)
+    except OSError:  # pragma: no cover
+        pass
     return {"value": done / dt, "unit": "drafts/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{done} single-sequence oracle steps over sequences 0..{min(done, cfg.B) - 1} "
-                      f"of the same {cfg.B}-sequence batch, {dt:.1f} s"}
+                      f"of the same {cfg.B}-sequence batch, {dt:.1f} s",
+            "cpu": cpu, "cores_available": len(os.sched_getaffinity(0))}
 
 
 def main():
