@@ -30,8 +30,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "5c5a516760cb1a29d5506846c16715a551cbd6080f25134b5854f1df43c08a80",
-    "fetch_kib": 267331.4,
+    "source_sha256": "6a93d7e251e3e403c4335b4683fd98116e5f1878733253cc2cf80f91263366ab",
+    "fetch_kib": 266488.0,
     "write_kib": 5392.0,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
