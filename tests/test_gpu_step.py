@@ -22,11 +22,12 @@ def host(bf):
             for f in FIELDS}
 
 
-@pytest.mark.parametrize("kw,split", [
-    (dict(B=3, L=300, d=256, k=6, W=3, S=5, seed=301, forced_every=2), False),
-    (dict(B=2, L=3000, d=128, Hq=8, Hkv=2, k=8, W=4, S=8, seed=302, forced_every=2), True),
+@pytest.mark.parametrize("kw,split,preceding", [
+    (dict(B=3, L=300, d=256, k=6, W=3, S=5, seed=301, forced_every=2), False, False),
+    (dict(B=2, L=3000, d=128, Hq=8, Hkv=2, k=8, W=4, S=8, seed=302, forced_every=2), True, False),
+    (dict(B=3, L=300, d=256, k=6, W=3, S=5, seed=303, forced_every=2), False, True),
 ])
-def test_native_step_matches_four_calls(kw, split):
+def test_native_step_matches_four_calls(kw, split, preceding):
     cfg = small_config(**kw)
     plan = adapld.verify_plan(cfg.B, cfg.L, cfg.T_max, cfg.Hq, cfg.Hkv)
     assert (plan["nsplit"] > 1) == split, plan
@@ -35,7 +36,7 @@ def test_native_step_matches_four_calls(kw, split):
              k_ctx=dev_bf16(x["k_ctx"]), v_ctx=dev_bf16(x["v_ctx"]), k_tree=dev_bf16(x["k_tree"]),
              v_tree=dev_bf16(x["v_tree"]))
     args = (t["tokens"], t["lens"], t["bank"], t["q"], t["k_ctx"], t["v_ctx"], t["k_tree"], t["v_tree"])
-    kw2 = dict(n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S)
+    kw2 = dict(n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, preceding=preceding)
     ref = host(adapld.step_calls(*args, **kw2))
     call = adapld.StepCall(*args, **kw2)
     for rep in range(2):   # the marshalled call replayed

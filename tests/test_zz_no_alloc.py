@@ -1,7 +1,8 @@
 """adapld_step_noalloc (the step with the library's own device workspace,
 for callers that cannot allocate) against adapld_step with a caller
 workspace: every output bit for bit, on two calls in a row, the second with
-a smaller input (the array keeps the first call's contents)."""
+a smaller input (the array keeps the first call's contents), then the
+smaller input again with Eq. (6)'s alignment of the rerank."""
 import numpy as np
 import pytest
 import torch
@@ -16,21 +17,22 @@ FIELDS = ("cand_pos", "cand_count", "match_n", "topk_pos", "topk_score", "topk_c
           "node_parent", "node_depth", "node_src", "node_count", "tree_mask", "out", "lse")
 
 
-def _step(x, cfg, noalloc):
+def _step(x, cfg, noalloc, preceding=False):
     args = [dev_i32(x["tokens"]), dev_i32(x["lens"]), dev_bf16(x["bank"]), dev_bf16(x["q"]),
             dev_bf16(x["k_ctx"]), dev_bf16(x["v_ctx"]), dev_bf16(x["k_tree"]), dev_bf16(x["v_tree"])]
     bufs = adapld.StepBuffers.allocate(cfg.B, cfg.L, cfg.d, cfg.k, cfg.T_max, cfg.Hq, cfg.Hkv, cfg.D)
     for name in FIELDS:   # outputs start as garbage that differs between the two runs
         t = getattr(bufs, name)
         t.view(torch.uint8).fill_(0x5A if noalloc else 0xA5)
-    adapld.step(*args, n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, buffers=bufs, noalloc=noalloc)
+    adapld.step(*args, n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, buffers=bufs, noalloc=noalloc,
+                preceding=preceding)
     torch.cuda.synchronize()
     return bufs
 
 
-def _compare(x, cfg, ctx):
-    ref = _step(x, cfg, False)
-    got = _step(x, cfg, True)
+def _compare(x, cfg, ctx, preceding=False):
+    ref = _step(x, cfg, False, preceding)
+    got = _step(x, cfg, True, preceding)
     B, L = cfg.B, cfg.L
     lens = np.clip(x["lens"], 0, L)
     cc = ref.cand_count.cpu().numpy()
@@ -64,4 +66,6 @@ def test_noalloc_step_two_calls():
     # second call: smaller, ragged, lexical hits and misses
     small = small_config(B=3, L=700, d=256, k=4, n_max=3, seed=302, V=40, Hq=8, Hkv=2, W=3, S=4,
                          forced_every=2)
-    _compare(make_inputs(small, lens=np.array([700, 333, 2], np.int32)), small, "second (smaller)")
+    xs = make_inputs(small, lens=np.array([700, 333, 2], np.int32))
+    _compare(xs, small, "second (smaller)")
+    _compare(xs, small, "third (smaller, rows j-1 against row L-2)", preceding=True)
