@@ -3,19 +3,31 @@
 // [0, L-2] whose token embedding has cosine >= tau with the embedding of the
 // last token; the hidden-state rerank of Sec. 3.4 then ranks them.
 //
-// flags kernel: workgroups of 4 waves tile the positions of every sequence
-// whose lexical set is empty, 16 positions per wave.  A wave holds the anchor
-// embedding in registers, reads the 16 token ids with one load, gathers the
-// embedding row of each position's token (two rows in flight, 16-byte
-// coalesced loads; rows of frequent tokens come from L2 and the last-level
-// cache, so HBM sees roughly one read per distinct token), reduces the dot
-// product and the squared norm with the same fixed DPP butterfly as the
-// hidden-state scan, and writes one flag byte per position.
+// The cosine of a position depends on its token only, so the test is taken
+// once per distinct token of the context (a quarter of the positions at
+// L = 8192 in Zipf-distributed text), in three kernels:
 //
-// compact kernel: one workgroup per sequence writes the candidate set in
-// ascending order (a non-empty lexical set is copied through), its size and
-// its kind, with per-thread runs of 32 flags and a wave + workgroup scan of
-// the run counts (as the lexical kernel orders its hits).
+// set kernel: one workgroup per sequence whose lexical set is empty marks
+// the tokens of its positions in a bitmap of the vocabulary held in LDS and
+// writes the distinct tokens (into the space of the candidate list, which is
+// written last).
+//
+// flags kernel: workgroups of 4 waves tile the distinct tokens, 16 per wave.
+// A wave holds the anchor embedding in registers, reads its 16 token ids
+// with one load, gathers each token's embedding row (two rows in flight,
+// 16-byte coalesced loads), reduces the dot product and the squared norm
+// with the same fixed DPP butterfly as the hidden-state scan, and writes one
+// flag byte per distinct token.
+//
+// compact kernel: one workgroup per sequence turns the flags into a bitmap of
+// the passing tokens in LDS, then writes the candidate set in ascending
+// position order (a non-empty lexical set is copied through), its size and
+// its kind, with per-thread runs of 32 positions and a wave + workgroup scan
+// of the run counts (as the lexical kernel orders its hits).
+//
+// A vocabulary too large for the LDS bitmap (more than kSetMaxV tokens) takes
+// the same flags kernel over positions instead of distinct tokens, and a
+// compaction of per-position flag bytes.
 //
 // The rerank is the hidden-state scan and merge kernels in rerank-only mode.
 //
@@ -33,11 +45,15 @@ namespace adapld {
 namespace {
 
 constexpr int kFlagWaves = 4;
-constexpr int kPosPerWave = 16;
-constexpr int kPosPerWg = kFlagWaves * kPosPerWave;
+constexpr int kPosPerWave = 16;                                // positions per wave
+constexpr int kSetPerWave = 4;                                 // distinct tokens per wave: each row
+                                                               // is a first touch, so more waves
 constexpr int kCompactThreads = 1024;
 constexpr int kCompactRun = 32;                                 // flags per thread per piece
 constexpr int kCompactPiece = kCompactThreads * kCompactRun;
+constexpr int kSetMaxV = 1 << 20;                            // vocabulary bitmap: 128 KiB of LDS
+constexpr int kSetBatch = 8;                                  // token loads in flight per thread
+constexpr int kSetRun = 4;                                    // positions per thread per compaction round
 
 struct EmbedArgs {
   const int32_t* tokens;
@@ -58,7 +74,9 @@ struct EmbedArgs {
 
 // cos(emb[t], anchor) >= tau for one gathered row; a token outside [0, V) has
 // a zero embedding (cosine 0).
-template <int NIT>
+// SET: the items are list v's distinct tokens (the set kernel's list and
+// count); otherwise its positions [pos_off, L - 1).
+template <int NIT, bool SET>
 __global__ __launch_bounds__(kFlagWaves * kWave) void embed_flags_kernel(const EmbedArgs a) {
   const int v = blockIdx.y;
   const int b = v / a.seq_div;
@@ -66,15 +84,18 @@ __global__ __launch_bounds__(kFlagWaves * kWave) void embed_flags_kernel(const E
   const int wave = threadIdx.x / kWave;
   if (a.skip[v] != 0) return;        // e.g. a lexical hit needs no flags
   const int L = min(max(a.lens[b], 0), a.L_stride);
-  const int J = L - 1 - a.pos_off;   // flags [0, J): positions [pos_off, L - 1)
-  const int j0 = blockIdx.x * kPosPerWg + wave * kPosPerWave;
+  const int n_pos = L - 1 - a.pos_off;
+  const int J = SET ? min(a.out_count[v], n_pos) : n_pos;   // flags [0, J)
+  constexpr int kPer = SET ? kSetPerWave : kPosPerWave;
+  const int j0 = (blockIdx.x * kFlagWaves + wave) * kPer;
   if (j0 >= J) return;
   const int32_t* __restrict__ M = a.tokens + (size_t)b * a.L_stride;
+  const int32_t* __restrict__ items = SET ? a.out_pos + (size_t)v * a.L_stride : M + a.pos_off;
   const int d = a.d;
 
   const int at = a.qtok ? a.qtok[v] : M[L - 1];
   const bool a_ok = at >= 0 && at < a.V;
-  const int my_tok = lane < kPosPerWave && j0 + lane < J ? M[j0 + lane + a.pos_off] : -1;
+  const int my_tok = lane < kPer && j0 + lane < J ? items[j0 + lane] : -1;
   uint4 qv[NIT];
   float qn = 0.f;
 #pragma unroll
@@ -106,7 +127,7 @@ __global__ __launch_bounds__(kFlagWaves * kWave) void embed_flags_kernel(const E
     }
   };
   uint8_t* __restrict__ fl = a.flags + (size_t)v * a.flag_stride;
-  const int n = min(kPosPerWave, J - j0);
+  const int n = min(kPer, J - j0);
   for (int i = 0; i < n; i += 2) {
     uint4 r0[NIT], r1[NIT];
     const int t0 = __builtin_amdgcn_readlane(my_tok, i);
@@ -184,24 +205,210 @@ __global__ __launch_bounds__(kCompactThreads) void embed_compact_kernel(const Em
   }
 }
 
+// Exclusive prefix of cnt over the workgroup's threads in order; *total gets the sum.
+__device__ __forceinline__ int block_excl_scan(int cnt, int* s_red, int* total) {
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  const int incl = wave_incl_scan_i32(cnt);
+  __syncthreads();   // earlier reads of s_red are done
+  if (lane == kWave - 1) s_red[wave] = incl;
+  __syncthreads();
+  int before = 0, sum = 0;
+#pragma unroll
+  for (int w = 0; w < kCompactThreads / kWave; ++w) {
+    const int c = s_red[w];
+    before += w < wave ? c : 0;
+    sum += c;
+  }
+  *total = sum;
+  return before + incl - cnt;
+}
+
+// The distinct tokens in [0, V) of list v's positions, in no particular
+// order, into out_pos (row v) and their number into out_count[v].  The first batch of
+// token loads is issued with the list's skip flag and length, before either
+// is known (indices clamped to the row), so the kernel starts with one
+// memory round trip.
+__global__ __launch_bounds__(kCompactThreads) void embed_set_kernel(const EmbedArgs a) {
+  __shared__ uint32_t s_bits[kSetMaxV / 32];
+  __shared__ int s_count;
+  const int v = blockIdx.x;
+  const int b = v / a.seq_div;
+  const int tid = threadIdx.x;
+  // Position i's token is M[i]; M[min(i, last)] stays inside the row.
+  const int32_t* __restrict__ M = a.tokens + (size_t)b * a.L_stride + a.pos_off;
+  const int last = a.L_stride - 1 - a.pos_off;
+  const int skip = a.skip[v];
+  const int L = min(max(a.lens[b], 0), a.L_stride);
+  int t[kSetBatch];
+#pragma unroll
+  for (int r = 0; r < kSetBatch; ++r) t[r] = M[min(r * kCompactThreads + tid, last)];
+  if (skip != 0) return;
+  const int J = max(L - 1 - a.pos_off, 0);
+  const int nwords = (a.V + 31) >> 5;
+  for (int i = tid; i < nwords; i += kCompactThreads) s_bits[i] = 0u;
+  if (tid == 0) s_count = 0;
+  __syncthreads();
+  for (int i0 = 0; i0 < J; i0 += kSetBatch * kCompactThreads) {
+    if (i0 > 0) {
+#pragma unroll
+      for (int r = 0; r < kSetBatch; ++r) t[r] = M[min(i0 + r * kCompactThreads + tid, last)];
+    }
+#pragma unroll
+    for (int r = 0; r < kSetBatch; ++r) {
+      const int x = t[r];
+      if (i0 + r * kCompactThreads + tid < J && x >= 0 && x < a.V) {
+        const uint32_t bit = 1u << (x & 31);
+        if ((s_bits[x >> 5] & bit) == 0u) atomicOr(&s_bits[x >> 5], bit);
+      }
+    }
+  }
+  __syncthreads();
+  // Rounds of one bitmap word per thread (frequent tokens have small ids, so
+  // a thread owning a run of words could hold hundreds of tokens).  The list
+  // is a set: a wave takes its slots with one LDS atomic, in whatever order
+  // the waves arrive, and lanes write their tokens at the wave's prefix.
+  int32_t* __restrict__ out = a.out_pos + (size_t)v * a.L_stride;
+  const int lane = lane_id();
+  for (int w0 = 0; w0 < nwords; w0 += kCompactThreads) {
+    const int w = w0 + tid;
+    uint32_t bits = w < nwords ? s_bits[w] : 0u;
+    const int cnt = __popc(bits);
+    const int incl = wave_incl_scan_i32(cnt);
+    const int wave_cnt = __builtin_amdgcn_readlane(incl, kWave - 1);
+    int base = 0;
+    if (lane == 0 && wave_cnt > 0) base = atomicAdd(&s_count, wave_cnt);
+    int slot = __builtin_amdgcn_readfirstlane(base) + incl - cnt;
+    while (bits) {
+      const int e = __builtin_ctz(bits);
+      bits &= bits - 1;
+      out[slot++] = (w << 5) + e;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) a.out_count[v] = s_count;
+}
+
+// The candidate set from the flags of the distinct tokens: a bitmap of the
+// tokens that pass, then the positions whose token is in it.  As in the set
+// kernel, the first loads of the token list, the flags and the positions'
+// tokens go out together with the list's skip flag, length and set size.
+__global__ __launch_bounds__(kCompactThreads) void embed_compact_set_kernel(const EmbedArgs a) {
+  __shared__ uint32_t s_bits[kSetMaxV / 32];
+  __shared__ int s_red[kCompactThreads / kWave];
+  const int v = blockIdx.x;
+  const int b = v / a.seq_div;
+  const int tid = threadIdx.x;
+  int32_t* __restrict__ out = a.out_pos + (size_t)v * a.L_stride;
+  const uint8_t* __restrict__ fl = a.flags + (size_t)v * a.flag_stride;
+  const int32_t* __restrict__ M = a.tokens + (size_t)b * a.L_stride + a.pos_off;
+  const int last = a.L_stride - 1 - a.pos_off;   // M[min(i, last)] stays inside the row
+  const int skip = a.skip[v];
+  const int L = min(max(a.lens[b], 0), a.L_stride);
+  const int n_set = a.out_count[v];
+  int st[kSetBatch];
+  uint32_t sf[kSetBatch];
+#pragma unroll
+  for (int r = 0; r < kSetBatch; ++r) {
+    const int i = min(r * kCompactThreads + tid, a.L_stride - 1);
+    st[r] = out[i];
+    sf[r] = fl[i];
+  }
+  int pt[kSetRun];   // the tokens of this thread's first positions
+#pragma unroll
+  for (int e = 0; e < kSetRun; ++e) pt[e] = M[min(tid * kSetRun + e, last)];
+  if (skip != 0) {
+    if (a.cand_pos) {   // the backoff rule: a lexical set is the result
+      const int cc = min(max(skip, 0), a.L_stride);
+      const int32_t* __restrict__ in = a.cand_pos + (size_t)v * a.L_stride;
+      for (int i = tid; i < cc; i += kCompactThreads) out[i] = in[i];
+      if (tid == 0) {
+        a.out_count[v] = cc;
+        if (a.out_kind) a.out_kind[v] = ADAPLD_KIND_LEX;
+      }
+    }
+    return;
+  }
+  const int J = max(L - 1 - a.pos_off, 0);
+  const int nwords = (a.V + 31) >> 5;
+  const int D = min(max(n_set, 0), J);   // distinct tokens, listed in out
+  for (int i = tid; i < nwords; i += kCompactThreads) s_bits[i] = 0u;
+  __syncthreads();
+  for (int i0 = 0; i0 < D; i0 += kSetBatch * kCompactThreads) {
+    if (i0 > 0) {
+#pragma unroll
+      for (int r = 0; r < kSetBatch; ++r) {
+        const int i = min(i0 + r * kCompactThreads + tid, D - 1);
+        st[r] = out[i];
+        sf[r] = fl[i];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kSetBatch; ++r)
+      if (i0 + r * kCompactThreads + tid < D && sf[r] != 0u) atomicOr(&s_bits[st[r] >> 5], 1u << (st[r] & 31));
+  }
+  __syncthreads();   // every read of the token list is done: out is rewritten below
+  const bool zero_passes = 0.f >= a.tau;   // a token outside [0, V): zero embedding, cosine 0
+  int total = 0;
+  for (int p0 = 0; p0 < J; p0 += kSetRun * kCompactThreads) {
+    // Thread tid owns positions [q0, q0 + kSetRun) of this round: neighbouring
+    // lanes read neighbouring tokens.
+    const int q0 = p0 + tid * kSetRun;
+    if (p0 > 0) {
+#pragma unroll
+      for (int e = 0; e < kSetRun; ++e) pt[e] = M[min(q0 + e, last)];
+    }
+    uint32_t bits = 0;
+#pragma unroll
+    for (int e = 0; e < kSetRun; ++e) {
+      const int x = pt[e];
+      const bool pass = x >= 0 && x < a.V ? ((s_bits[x >> 5] >> (x & 31)) & 1u) != 0u : zero_passes;
+      if (pass && q0 + e < J) bits |= 1u << e;
+    }
+    int round;
+    int slot = total + block_excl_scan(__popc(bits), s_red, &round);
+    while (bits) {
+      const int e = __builtin_ctz(bits);
+      bits &= bits - 1;
+      out[slot++] = q0 + e;
+    }
+    total += round;
+  }
+  if (tid == 0) {
+    a.out_count[v] = total;
+    if (a.out_kind) a.out_kind[v] = total > 0 ? ADAPLD_KIND_SEM : ADAPLD_KIND_NONE;
+  }
+}
+
 template <int NIT>
-void launch_flags(const EmbedArgs& a, int B, hipStream_t stream) {
-  const dim3 grid((a.L_stride + kPosPerWg - 1) / kPosPerWg, B);
-  hipLaunchKernelGGL(embed_flags_kernel<NIT>, grid, dim3(kFlagWaves * kWave), 0, stream, a);
+void launch_flags(const EmbedArgs& a, int B, bool set, hipStream_t stream) {
+  const int per_wg = kFlagWaves * (set ? kSetPerWave : kPosPerWave);
+  const dim3 grid((a.L_stride + per_wg - 1) / per_wg, B);
+  if (set)
+    hipLaunchKernelGGL((embed_flags_kernel<NIT, true>), grid, dim3(kFlagWaves * kWave), 0, stream, a);
+  else
+    hipLaunchKernelGGL((embed_flags_kernel<NIT, false>), grid, dim3(kFlagWaves * kWave), 0, stream, a);
 }
 
 size_t flag_stride_of(int L_stride) {
   return ((size_t)L_stride + kCompactRun - 1) / kCompactRun * kCompactRun;
 }
 
-// The flags kernel (one instantiation per 512-element slice count of d),
-// then the compaction.
+// The set kernel (vocabularies of up to kSetMaxV tokens), the flags kernel
+// (one instantiation per 512-element slice count of d), then the compaction.
 hipError_t launch_embed_lists(const EmbedArgs& a, int lists, hipStream_t stream) {
   const int nit = (a.d + 8 * kWave - 1) / (8 * kWave);
+  if (nit < 1 || nit > 16) return hipErrorInvalidValue;
+  const bool set = a.V <= kSetMaxV;
+  if (set) {
+    hipLaunchKernelGGL(embed_set_kernel, dim3(lists), dim3(kCompactThreads), 0, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   switch (nit) {
 #define ADAPLD_FLAGS_CASE(n) \
   case n:                    \
-    launch_flags<n>(a, lists, stream); \
+    launch_flags<n>(a, lists, set, stream); \
     break;
     ADAPLD_FLAGS_CASE(1) ADAPLD_FLAGS_CASE(2) ADAPLD_FLAGS_CASE(3) ADAPLD_FLAGS_CASE(4)
     ADAPLD_FLAGS_CASE(5) ADAPLD_FLAGS_CASE(6) ADAPLD_FLAGS_CASE(7) ADAPLD_FLAGS_CASE(8)
@@ -213,7 +420,10 @@ hipError_t launch_embed_lists(const EmbedArgs& a, int lists, hipStream_t stream)
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(embed_compact_kernel, dim3(lists), dim3(kCompactThreads), 0, stream, a);
+  if (set)
+    hipLaunchKernelGGL(embed_compact_set_kernel, dim3(lists), dim3(kCompactThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(embed_compact_kernel, dim3(lists), dim3(kCompactThreads), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -158,3 +158,46 @@ def test_embedding_fallback_threshold_equality(tau):
     assert on > 0, "no cosine sits exactly on tau"
     kinds = run_and_check(cfg, x, E_bits, tau, 64, f"tau={tau} exact", exact=True)
     assert oracle.KIND_SEM in kinds or oracle.KIND_NONE in kinds
+
+
+@pytest.mark.parametrize("V", [1 << 20, (1 << 20) + 5])
+def test_embedding_fallback_vocabulary_edge(V):
+    """The distinct-token path takes vocabularies of up to 2^20 tokens (a
+    bitmap of them in LDS), larger ones the per-position path: both around
+    that size, with ids at the last row of the table and just past it."""
+    cfg = small_config(B=4, L=600, d=64, k=64, n_max=3, seed=171, V=50, forced_every=1)
+    x = make_inputs(cfg, with_verify=False)
+    small = emb_table(cfg.V + 8, 64, clusters=5, seed=13)
+    E_bits = np.zeros((V, 64), dtype=np.uint16)
+    E_bits[:small.shape[0]] = small
+    E_bits[V - 1] = small[3]          # the last id is a near twin of id 3
+    rng = np.random.default_rng(5)
+    for b in range(cfg.B):
+        L = int(x["lens"][b])
+        idx = rng.choice(L - 1, size=16, replace=False)
+        x["tokens"][b, idx[:8]] = V - 1
+        x["tokens"][b, idx[8:]] = V   # outside the table: zero embedding
+    tokens, lens = dev_i32(x["tokens"]), dev_i32(x["lens"])
+    cp, cc, mn = adapld.lexical_match(tokens, lens, cfg.n_max)
+    # the oracle sees the ids past the table mapped to an extra zero row
+    E = oracle.bf16_bits_to_f64(np.concatenate([E_bits, np.zeros((1, 64), dtype=np.uint16)]))
+    taus = [t for t in (0.6, 0.55, 0.65) if margin_ok(E, x["tokens"], x["lens"], t)][:1] + \
+        [t for t in (-0.13, -0.27, -0.41, -0.07) if margin_ok(E, x["tokens"], x["lens"], t)][:1]
+    assert len(taus) == 2, "no threshold clear of the cosines present"
+    for tau in taus:
+        pos, sc, cnt, kind = adapld.semantic_topk_embed(dev_bf16(x["bank"]), tokens, lens, cp, cc,
+                                                        dev_bf16(E_bits), 64, tau)
+        torch.cuda.synchronize()
+        cnt, kind, pos = cnt.cpu().numpy(), kind.cpu().numpy(), pos.cpu().numpy()
+        sem = 0
+        for b in range(cfg.B):
+            L = int(x["lens"][b])
+            M = x["tokens"][b, :L]
+            _, C = oracle.lexical_match(M, cfg.n_max)
+            ekind, Cs = oracle.embedding_fallback(M, E, C, tau)
+            assert int(kind[b]) == ekind, (V, tau, b)
+            if ekind == oracle.KIND_SEM:
+                sem += 1
+                if len(Cs) <= 64:
+                    assert sorted(int(p) for p in pos[b, :int(cnt[b])]) == sorted(Cs), (V, tau, b)
+        assert sem > 0, (V, tau)
