@@ -1,0 +1,93 @@
+"""GPU parity of adapld_tree_verify_attn against the oracle's tree attention
+(Sec. 3.6) on every node of every sequence, on random branching trees (each
+node's parent any earlier node or the root), so that masks are arbitrary
+ancestor-or-self relations rather than the builder's chains.  Node counts
+and context lengths mix sequences whose stacked rows fill two row groups,
+one row group or none, ragged last tiles, contexts shorter than one tile or
+empty, and a batch with almost no work; the shape is the benchmark's
+(16 sequences, 32 query heads over 8 kv heads, T_max = 52)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_05742_amd as adapld
+from paper_2606_05742_amd.synth import f32_to_bf16_bits
+from parity_helpers import check_verify, dev_bf16, dev_i32
+
+pytestmark = pytest.mark.gpu
+
+B, HQ, HKV, D, T_MAX = 16, 32, 8, 128, 52   # 4 query heads per kv head: up to 208 stacked rows
+
+
+def random_tree(rng, T):
+    parent = np.full(T, -1, dtype=np.int64)
+    for u in range(1, T):
+        parent[u] = rng.integers(-1, u)
+    mask = np.zeros((T, T), dtype=bool)
+    for u in range(T):
+        v = u
+        while v >= 0:
+            mask[u, v] = True
+            v = parent[v]
+    return mask
+
+
+def run_case(L_stride, lens, counts, seed):
+    rng = np.random.default_rng(seed)
+    plan = adapld.verify_plan(B, L_stride, T_MAX, HQ, HKV)
+    assert (plan["kh"], plan["rowgroups"], plan["nsplit"]) == (2, 2, 1), plan   # the benchmark's decomposition
+    bits = lambda shape: f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32))  # noqa: E731
+    q = bits((B, T_MAX, HQ, D))
+    kc = bits((B, HKV, L_stride, D))
+    vc = bits((B, HKV, L_stride, D))
+    kt = bits((B, T_MAX, HKV, D))
+    vt = bits((B, T_MAX, HKV, D))
+    nw = (T_MAX + 63) // 64
+    masks = []
+    words = np.zeros((B, T_MAX, nw), dtype=np.uint64)
+    for b in range(B):
+        m = random_tree(rng, counts[b])
+        masks.append(m)
+        for u in range(counts[b]):
+            for v in range(counts[b]):
+                if m[u, v]:
+                    words[b, u, v // 64] |= np.uint64(1) << np.uint64(v % 64)
+    out, lse = adapld.tree_verify_attn(dev_bf16(q), dev_bf16(kc), dev_bf16(vc), dev_bf16(kt), dev_bf16(vt),
+                                       dev_i32(np.asarray(lens)), dev_i32(np.asarray(counts)),
+                                       torch.from_numpy(words.view(np.int64)).cuda())
+    torch.cuda.synchronize()
+    out = out.float().cpu().numpy()
+    lse = lse.cpu().numpy()
+    scale = 1.0 / math.sqrt(D)
+    for b in range(B):
+        T, L = counts[b], lens[b]
+        if T == 0:
+            continue
+        O, LSE = oracle.tree_verify_attn(
+            oracle.bf16_bits_to_f64(q[b, :T]), oracle.bf16_bits_to_f64(kc[b, :, :L]),
+            oracle.bf16_bits_to_f64(vc[b, :, :L]), oracle.bf16_bits_to_f64(kt[b, :T]),
+            oracle.bf16_bits_to_f64(vt[b, :T]), masks[b], L, scale)
+        check_verify(out[b, :T], lse[b, :, :T], O, LSE, f"seed={seed} b={b} T={T} L={L}")
+
+
+def test_random_trees_mixed_sizes():
+    # 208 and 140 stacked rows (two row groups), 128, 104 and 4 (one), none
+    counts = [52, 52, 35, 32, 26, 1, 0, 52, 13, 52, 40, 26, 33, 0, 52, 7]
+    lens = [700, 699, 640, 65, 64, 700, 700, 1, 0, 333, 700, 129, 700, 5, 700, 700]
+    run_case(700, lens, counts, seed=1)
+
+
+def test_random_trees_two_row_groups():
+    counts = [52] * 16
+    lens = [2048] * 16
+    run_case(2048, lens, counts, seed=2)
+
+
+def test_random_trees_almost_no_work():
+    """Two live sequences, contexts of 130 and 64 keys."""
+    counts = [33, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 20]
+    lens = [130, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 64]
+    run_case(200, lens, counts, seed=3)
