@@ -1,5 +1,6 @@
-"""The step captured in a HIP graph and replayed, both as four entry-point
-calls and as one adapld_step call.
+"""The step captured in a HIP graph and replayed: as four entry-point calls,
+as one adapld_step call, and as one adapld_step_noalloc call (the entry
+point for callers that cannot allocate, e.g. under graph capture).
 
 Every replay must reproduce the eager step bit for bit, also with other eager
 work (a different batch through the same buffers) and host synchronisations
@@ -43,6 +44,12 @@ def _run_native(cfg, bufs, d):
     adapld.step(*d, n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, buffers=bufs)
 
 
+def _run_noalloc(cfg, bufs, d):
+    # adapld_step_noalloc: the library's own device workspace, so the
+    # captured kernels hold its address
+    adapld.step(*d, n_max=cfg.n_max, k=cfg.k, W=cfg.W, S=cfg.S, buffers=bufs, noalloc=True)
+
+
 def _snapshot(bufs):
     return {n: getattr(bufs, n).clone() for n in OUTPUTS}
 
@@ -57,16 +64,16 @@ def _poison(bufs):
             t.fill_(-7 if t.dtype != torch.uint64 else 0)
 
 
-@pytest.mark.parametrize("native", [False, True])
+@pytest.mark.parametrize("mode", ["calls", "step", "noalloc"])
 @pytest.mark.parametrize("L", [700, 3000])
-def test_graph_replay_matches_eager(L, native):
+def test_graph_replay_matches_eager(L, mode):
     # L = 3000 with B = 2 splits the verify context (the combine kernel runs too).
     cfg = small_config(B=2, L=L, d=512, Hq=8, Hkv=2, k=8, W=4, S=6, n_max=3, seed=97, forced_every=2)
     other = small_config(B=2, L=L, d=512, Hq=8, Hkv=2, k=8, W=4, S=6, n_max=3, seed=98, forced_every=2)
     d = _upload(make_inputs(cfg))
     d_other = _upload(make_inputs(other))
     bufs = adapld.StepBuffers.allocate(cfg.B, cfg.L, cfg.d, cfg.k, cfg.T_max, cfg.Hq, cfg.Hkv, cfg.D)
-    run = _run_native if native else _run
+    run = {"calls": _run, "step": _run_native, "noalloc": _run_noalloc}[mode]
 
     _poison(bufs)
     run(cfg, bufs, d)
