@@ -5,7 +5,11 @@ ancestor-or-self relations rather than the builder's chains.  Node counts
 and context lengths mix sequences whose stacked rows fill two row groups,
 one row group or none, ragged last tiles, contexts shorter than one tile or
 empty, and a batch with almost no work; the shape is the benchmark's
-(16 sequences, 32 query heads over 8 kv heads, T_max = 52)."""
+(16 sequences, 32 query heads over 8 kv heads, T_max = 52), and three more
+shapes take the other decompositions: 40 query heads over 8 with T_max = 137
+(every wave its own block, three row groups), 64 over 8 with T_max = 72 and
+a split context (five row groups, the combine kernel), and 32 heads without
+grouping (one row group, split)."""
 import math
 
 import numpy as np
@@ -19,7 +23,7 @@ from parity_helpers import check_verify, dev_bf16, dev_i32
 
 pytestmark = pytest.mark.gpu
 
-B, HQ, HKV, D, T_MAX = 16, 32, 8, 128, 52   # 4 query heads per kv head: up to 208 stacked rows
+D = 128
 
 
 def random_tree(rng, T):
@@ -35,10 +39,13 @@ def random_tree(rng, T):
     return mask
 
 
-def run_case(L_stride, lens, counts, seed):
+def run_case(L_stride, lens, counts, seed, B=16, HQ=32, HKV=8, T_MAX=52, plan_is=(2, 2, 1)):
+    """plan_is: the decomposition the case must take (waves per row block,
+    row groups, splits; None for splits: more than one)."""
     rng = np.random.default_rng(seed)
     plan = adapld.verify_plan(B, L_stride, T_MAX, HQ, HKV)
-    assert (plan["kh"], plan["rowgroups"], plan["nsplit"]) == (2, 2, 1), plan   # the benchmark's decomposition
+    kh, rgs, ns = plan_is
+    assert (plan["kh"], plan["rowgroups"]) == (kh, rgs) and (plan["nsplit"] > 1 if ns is None else plan["nsplit"] == ns), plan
     bits = lambda shape: f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32))  # noqa: E731
     q = bits((B, T_MAX, HQ, D))
     kc = bits((B, HKV, L_stride, D))
@@ -91,3 +98,24 @@ def test_random_trees_almost_no_work():
     counts = [33, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 20]
     lens = [130, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 64]
     run_case(200, lens, counts, seed=3)
+
+
+def test_random_trees_every_wave_its_block():
+    """40 query heads over 8: up to 685 stacked rows in row groups of 256."""
+    counts = [137, 1, 0, 64, 100, 137, 52, 77]
+    lens = [1500, 1500, 700, 1, 64, 1499, 900, 1500]
+    run_case(1500, lens, counts, seed=4, B=8, HQ=40, HKV=8, T_MAX=137, plan_is=(1, 3, 1))
+
+
+def test_random_trees_split_context():
+    """64 query heads over 8, five row groups, the context split in two."""
+    counts = [72, 9, 0]
+    lens = [5000, 4999, 5000]
+    run_case(5000, lens, counts, seed=5, B=3, HQ=64, HKV=8, T_MAX=72, plan_is=(2, 5, None))
+
+
+def test_random_trees_no_grouping():
+    """32 heads, each its own kv head (G = 1), split context."""
+    counts = [30, 17]
+    lens = [900, 300]
+    run_case(900, lens, counts, seed=6, B=2, HQ=32, HKV=32, T_MAX=30, plan_is=(2, 1, None))
