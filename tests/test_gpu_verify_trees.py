@@ -9,7 +9,8 @@ empty, and a batch with almost no work; the shape is the benchmark's
 shapes take the other decompositions: 40 query heads over 8 with T_max = 137
 (every wave its own block, three row groups), 64 over 8 with T_max = 72 and
 a split context (five row groups, the combine kernel), and 32 heads without
-grouping (one row group, split)."""
+grouping (one row group, split); the last case is the largest tree the
+boundary takes (256 nodes)."""
 import math
 
 import numpy as np
@@ -119,3 +120,11 @@ def test_random_trees_no_grouping():
     counts = [30, 17]
     lens = [900, 300]
     run_case(900, lens, counts, seed=6, B=2, HQ=32, HKV=32, T_MAX=30, plan_is=(2, 1, None))
+
+
+def test_random_trees_largest():
+    """T_max = 256, the largest tree the boundary takes: four tree tiles and
+    four mask words per row, a 256-node tree beside smaller ones."""
+    counts = [256, 200, 65]
+    lens = [700, 0, 64]
+    run_case(700, lens, counts, seed=7, B=3, HQ=16, HKV=16, T_MAX=256, plan_is=(2, 2, 1))
