@@ -212,6 +212,32 @@ def test_lexical_single_piece_runs(L, n_max):
     assert int(mn[0]) == n_max and int(mn[1]) == n_max
 
 
+@pytest.mark.parametrize("L,n_max", [(5000, 17), (5000, 33), (5000, 64), (40000, 64)])
+def test_lexical_longest_ngrams(L, n_max):
+    """n-gram bounds above 16, up to the boundary's largest (64), in one LDS
+    piece and in several: an 80-token repeat of the query suffix makes
+    n* = n_max, and a second copy shortened by one token must not count."""
+    cfg = small_config(B=2, L=L, d=8, n_max=n_max, seed=96, V=40, copy_frac=0.3, span=(8, 64))
+    x = make_inputs(cfg, with_bank=False, with_verify=False)
+    t = x["tokens"]
+    x["lens"][:] = [L, L - 77]
+    for b in range(2):
+        Lb = int(x["lens"][b])
+        t[b, Lb // 3:Lb // 3 + 80] = t[b, Lb - 80:Lb]               # full repeat: n* = n_max
+        t[b, Lb // 2:Lb // 2 + 80] = t[b, Lb - 80:Lb]
+        t[b, Lb // 2 + 80 - 64 - 1] = -1                              # breaks the second copy's 64-gram
+    lens = dev_i32(x["lens"])
+    cp, cc, mn = adapld.lexical_match(dev_i32(t), lens, n_max)
+    torch.cuda.synchronize()
+    cp, cc, mn = cp.cpu().numpy(), cc.cpu().numpy(), mn.cpu().numpy()
+    for b in range(2):
+        Lb = int(x["lens"][b])
+        n, C = oracle.lexical_match(t[b, :Lb], n_max)
+        assert n == n_max, (b, n)
+        assert int(mn[b]) == n and int(cc[b]) == len(C), (b, int(mn[b]), n, int(cc[b]), len(C))
+        np.testing.assert_array_equal(cp[b, :len(C)], C)
+
+
 # Shapes that take each verify decomposition (tests/test_abi.py checks the
 # plan): 256-row workgroups whole and split, 128-row wave-pair workgroups
 # whole and split.  The first has 260 stacked rows, so its second row group
