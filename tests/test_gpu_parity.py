@@ -238,6 +238,30 @@ def test_lexical_longest_ngrams(L, n_max):
         np.testing.assert_array_equal(cp[b, :len(C)], C)
 
 
+def test_semantic_largest_batch():
+    """2048 sequences, the most one adapld_semantic_topk call takes (the scan
+    partitions all their rows over its 1024 waves and the merge runs one
+    workgroup per sequence): ragged short contexts, lexical hits and misses."""
+    cfg = small_config(B=2048, L=40, d=64, k=8, n_max=2, seed=97, V=300, forced_every=3)
+    lens = np.random.default_rng(5).integers(0, 41, size=cfg.B).astype(np.int32)
+    x = make_inputs(cfg, lens=lens, with_verify=False)
+    tokens, dlens = dev_i32(x["tokens"]), dev_i32(x["lens"])
+    cp, cc, mn = adapld.lexical_match(tokens, dlens, cfg.n_max)
+    pos, sc, cnt, kind = adapld.semantic_topk(dev_bf16(x["bank"]), dlens, cp, cc, cfg.k)
+    torch.cuda.synchronize()
+    cc, pos, sc, cnt, kind = (t.cpu().numpy() for t in (cc, pos, sc, cnt, kind))
+    kinds = set()
+    for b in range(cfg.B):
+        L = int(x["lens"][b])
+        _, C = oracle.lexical_match(x["tokens"][b, :L], cfg.n_max)
+        assert int(cc[b]) == len(C), b
+        n = int(cnt[b])
+        check_ranked(oracle.bf16_bits_to_f64(x["bank"][b, :L]), None, C, cfg.k, None, int(kind[b]),
+                     [int(p) for p in pos[b, :n]], [float(v) for v in sc[b, :n]], f"b={b}")
+        kinds.add(int(kind[b]))
+    assert kinds >= {adapld.KIND_LEX, adapld.KIND_SEM, adapld.KIND_NONE}, kinds
+
+
 # Shapes that take each verify decomposition (tests/test_abi.py checks the
 # plan): 256-row workgroups whole and split, 128-row wave-pair workgroups
 # whole and split.  The first has 260 stacked rows, so its second row group
