@@ -12,9 +12,10 @@
 // writes the distinct tokens (into the space of the candidate list, which is
 // written last).
 //
-// flags kernel: workgroups of 4 waves tile the distinct tokens, 16 per wave.
-// A wave holds the anchor embedding in registers, reads its 16 token ids
-// with one load, gathers each token's embedding row (two rows in flight,
+// flags kernel: workgroups of 4 waves tile the distinct tokens, 4 per wave
+// (each row is a first touch from HBM, so many waves share the latency).
+// A wave holds the anchor embedding in registers, reads its token ids with
+// one load, gathers each token's embedding row (two rows in flight,
 // 16-byte coalesced loads), reduces the dot product and the squared norm
 // with the same fixed DPP butterfly as the hidden-state scan, and writes one
 // flag byte per distinct token.
@@ -22,16 +23,16 @@
 // compact kernel: one workgroup per sequence turns the flags into a bitmap of
 // the passing tokens in LDS, then writes the candidate set in ascending
 // position order (a non-empty lexical set is copied through), its size and
-// its kind, with per-thread runs of 32 positions and a wave + workgroup scan
-// of the run counts (as the lexical kernel orders its hits).
+// its kind, in rounds of 4 consecutive positions per thread with a wave +
+// workgroup scan of the counts (as the lexical kernel orders its hits).
 //
 // A vocabulary too large for the LDS bitmap (more than kSetMaxV tokens) takes
-// the same flags kernel over positions instead of distinct tokens, and a
-// compaction of per-position flag bytes.
+// the same flags kernel over positions instead of distinct tokens (16 per
+// wave), and a compaction of per-position flag bytes in runs of 32.
 //
 // The rerank is the hidden-state scan and merge kernels in rerank-only mode.
 //
-// The same two kernels serve the successor retrieval of the paper's draft
+// The same kernels serve the successor retrieval of the paper's draft
 // construction (Sec. 3.5): there a "list" is one branch token of one
 // sequence, its query is the branch token's embedding, its positions are the
 // occurrence candidates t in [1, L-2] (flag index t - 1, the rerank row of
@@ -45,13 +46,12 @@ namespace adapld {
 namespace {
 
 constexpr int kFlagWaves = 4;
-constexpr int kPosPerWave = 16;                                // positions per wave
-constexpr int kSetPerWave = 4;                                 // distinct tokens per wave: each row
-                                                               // is a first touch, so more waves
+constexpr int kPosPerWave = 16;                               // positions per wave
+constexpr int kSetPerWave = 4;                                // distinct tokens per wave
 constexpr int kCompactThreads = 1024;
-constexpr int kCompactRun = 32;                                 // flags per thread per piece
+constexpr int kCompactRun = 32;                               // flags per thread per piece
 constexpr int kCompactPiece = kCompactThreads * kCompactRun;
-constexpr int kSetMaxV = 1 << 20;                            // vocabulary bitmap: 128 KiB of LDS
+constexpr int kSetMaxV = 1 << 20;                             // vocabulary bitmap: 128 KiB of LDS
 constexpr int kSetBatch = 8;                                  // token loads in flight per thread
 constexpr int kSetRun = 4;                                    // positions per thread per compaction round
 
