@@ -13,10 +13,10 @@
 // copied once per sequence.
 //
 // successor backoff (with an embedding table): a branch token that never
-// occurs in [1, L-2] takes instead the positions whose token embedding is
-// within tau of its own (Sec. 3.5 applies the lexical-first backoff of
-// Sec. 3.3 to the successor query), from the embedding flag and compaction
-// kernels run over the B*W lists.
+// occurs in [1, L-2] takes instead the positions whose token embedding has
+// cosine >= tau with its own (Sec. 3.5 applies the lexical-first backoff of
+// Sec. 3.3 to the successor query), from the embedding fallback's kernels
+// run over the B*W lists.
 //
 // Successors are drafted for every branch (the text of Sec. 3.5) or only
 // after a semantic anchor (Algorithm 1's strict branch drafts none),
