@@ -22,6 +22,15 @@
 // overflow are copied by the whole workgroup, and every thread writes its
 // position at its rank inside its group, so every array stays ascending.
 //
+// append kernel: one workgroup per sequence, one wave per level, each wave
+// inserting its level's new positions 64 at a time (a register bitonic sort
+// of hash bits and index forms the groups; a batch holding two different
+// n-grams with equal bits falls back to one position at a time); a level that
+// was never built, or whose context shrank or pool overflowed, is rebuilt
+// from scratch by its wave.  With the match fused in, the first
+// wave then answers the lexical match from the levels just brought up to
+// date, so an iteration costs one launch.
+//
 // match kernel: one workgroup per sequence; lane n-1 of the first wave looks
 // up the last n tokens at level n, the longest level with a hit gives n*,
 // and its array is copied out as C_lex: one contiguous read.
