@@ -10,8 +10,9 @@
 // the mix of fallbacks and hits.
 //
 // scan kernel: each wave streams its range from HBM into a private LDS ring
-// with direct-to-LDS loads (global_load_lds_dwordx4; up to kScanRingBytes in
-// flight per wave, no register staging), reads each row back with 16-byte LDS
+// with direct-to-LDS loads (global_load_lds_dwordx4 with the non-temporal
+// hint, since every row is read once; up to kScanRingBytes in flight per
+// wave, no register staging), reads each row back with 16-byte LDS
 // reads (lane l holds elements 8*(l + 64*i) .. +7), holds the query slice for
 // those elements in registers, accumulates the dot product and the squared
 // norm in fp32 with v_dot2c_f32_bf16 and reduces them with fixed DPP
@@ -197,7 +198,7 @@ __global__ __launch_bounds__(kScanThreads, 1) void semantic_scan_kernel(const Sc
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
       const int e = (it * kWave + lane) * 8;
-      dma16(row + (e < d ? e : 0), ring + slot * kSlotBytes + it * 1024);
+      dma16_stream(row + (e < d ? e : 0), ring + slot * kSlotBytes + it * 1024);
     }
   };
 
