@@ -30,8 +30,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "6a93d7e251e3e403c4335b4683fd98116e5f1878733253cc2cf80f91263366ab",
-    "fetch_kib": 266488.0,
+    "source_sha256": "d5f455140ad48d6805bcd649de474f4b807228ac9e2d23bb457e3898550b72ed",
+    "fetch_kib": 266414.1,
     "write_kib": 5392.0,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
