@@ -51,7 +51,7 @@ def test_workspace_sizes(lib):
     assert ws(2, 16, 300, 4096, 8, 0, 0, 0, 0) == 16 * 300 * 8 * 8  # at most one per row
     assert ws(2, 16, 8192, 4096, 65, 0, 0, 0, 0) == 0              # k beyond the limit
     assert ws(4, 1, 4096, 0, 0, 44, 32, 8, 128) > 0                # split context
-    assert ws(4, 16, 8192, 0, 0, 52, 32, 8, 128) == 0              # one split: no partials
+    assert ws(4, 16, 2048, 0, 0, 52, 32, 8, 128) == 0              # one split: no partials
     assert ws(4, 16, 8192, 0, 0, 52, 32, 7, 128) == 0              # Hq % Hkv != 0
     assert ws(9, 16, 8192, 0, 0, 52, 32, 8, 128) == 0
 

@@ -9,7 +9,8 @@ empty, and a batch with almost no work; the shape is the benchmark's
 shapes take the other decompositions: 40 query heads over 8 with T_max = 137
 (every wave its own block, three row groups), 64 over 8 with T_max = 72 and
 a split context (five row groups, the combine kernel), and 32 heads without
-grouping (one row group, split); the last case is the largest tree the
+grouping (one row group, split); a case at 8192 keys takes whole-workgroup
+row blocks in one row group with a split context; the last case is the largest tree the
 boundary takes (256 nodes)."""
 import math
 
@@ -113,6 +114,15 @@ def test_random_trees_split_context():
     counts = [72, 9, 0]
     lens = [5000, 4999, 5000]
     run_case(5000, lens, counts, seed=5, B=3, HQ=64, HKV=8, T_MAX=72, plan_is=(2, 5, None))
+
+
+def test_random_trees_one_row_group_streaming():
+    """The benchmark's heads at 8192 keys and 4 sequences: whole-workgroup row
+    blocks, one row group (its tiles loaded with the streaming hint), the
+    context split in eight, ragged last tiles."""
+    counts = [52, 52, 30, 1]
+    lens = [8192, 8191, 4097, 100]
+    run_case(8192, lens, counts, seed=8, B=4, HQ=32, HKV=8, T_MAX=52, plan_is=(1, 1, None))
 
 
 def test_random_trees_no_grouping():
