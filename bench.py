@@ -30,9 +30,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "d5f455140ad48d6805bcd649de474f4b807228ac9e2d23bb457e3898550b72ed",
-    "fetch_kib": 266414.1,
-    "write_kib": 5392.0,
+    "source_sha256": "639a35c13f128425cb7d3cc6c3545beeb146127762b02ca30357d1c8580dcc76",
+    "fetch_kib": 276121.8,
+    "write_kib": 16567.6,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
 }

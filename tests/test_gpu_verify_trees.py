@@ -8,9 +8,10 @@ empty, and a batch with almost no work; the shape is the benchmark's
 (16 sequences, 32 query heads over 8 kv heads, T_max = 52), and three more
 shapes take the other decompositions: 40 query heads over 8 with T_max = 137
 (every wave its own block, three row groups), 64 over 8 with T_max = 72 and
-a split context (five row groups, the combine kernel), and 32 heads without
-grouping (one row group, split); a case at 8192 keys takes whole-workgroup
-row blocks in one row group with a split context; the last case is the largest tree the
+a split context (five row groups, two splits), and 32 heads without
+grouping (one row group, four splits); two cases at 8192 keys take
+whole-workgroup row blocks in one row group with four and eight splits;
+the last case is the largest tree the
 boundary takes (256 nodes)."""
 import math
 
@@ -117,12 +118,20 @@ def test_random_trees_split_context():
 
 
 def test_random_trees_one_row_group_streaming():
-    """The benchmark's heads at 8192 keys and 4 sequences: whole-workgroup row
+    """The benchmark's heads at 8192 keys and 8 sequences: whole-workgroup row
     blocks, one row group (its tiles loaded with the streaming hint), the
-    context split in eight, ragged last tiles."""
-    counts = [52, 52, 30, 1]
-    lens = [8192, 8191, 4097, 100]
-    run_case(8192, lens, counts, seed=8, B=4, HQ=32, HKV=8, T_MAX=52, plan_is=(1, 1, None))
+    context split in four, ragged last tiles, a context that ends inside the
+    first split (three splits with no key)."""
+    counts = [52, 52, 30, 1, 52, 17, 0, 52]
+    lens = [8192, 8191, 4097, 100, 2048, 6000, 8192, 1]
+    run_case(8192, lens, counts, seed=8, B=8, HQ=32, HKV=8, T_MAX=52, plan_is=(1, 1, 4))
+
+
+def test_random_trees_eight_splits():
+    """4 sequences of 8192 keys: eight splits."""
+    counts = [52, 40, 1, 52]
+    lens = [8192, 8000, 64, 1000]
+    run_case(8192, lens, counts, seed=9, B=4, HQ=32, HKV=8, T_MAX=52, plan_is=(1, 1, 8))
 
 
 def test_random_trees_no_grouping():
