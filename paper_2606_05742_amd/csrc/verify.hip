@@ -664,29 +664,33 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void tree_verify_kernel(const Ver
   }
 }
 
-// Merge the splits: 8 stacked rows per workgroup, 32 threads x 4 dims per row.
-__global__ __launch_bounds__(256) void verify_combine_kernel(const VerifyArgs a) {
-  const int qr = blockIdx.x * 8 + (threadIdx.x >> 5);
+// Merge the splits: 8 stacked rows per workgroup, 16 threads x 8 dims (one
+// 16-byte load per split) per row.
+constexpr int kCombineRows = 8;
+__global__ __launch_bounds__(kCombineRows * 16) void verify_combine_kernel(const VerifyArgs a) {
+  const int qr = blockIdx.x * kCombineRows + (threadIdx.x >> 4);
   const int bg = blockIdx.y;
   if (qr >= a.rows_max) return;
-  const int dim = (threadIdx.x & 31) * 4;
+  const int dim = (threadIdx.x & 15) * 8;
   const size_t row0 = (size_t)bg * a.nsplit * a.rows_max + qr;   // split 0 of this row
+  const int b = bg / a.Hkv;
+  const int T = min(max(a.node_count[b], 0), a.T_max);
   // One pass over the splits in index order, four at a time.  The maxima and
   // partials of a group are loaded together, and before node_count is known
   // (every slot is in bounds), so a call with up to four splits costs one
   // memory round trip; the running max moves online.  Split s carries O_s/l_s
   // with weight l_s 2^(m_s - M).
   float M = -INFINITY, den = 0.f;
-  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  float num[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < a.nsplit; s0 += 4) {
     float2 ml[4];
-    uint2 v[4];
+    uint4 v[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const bool in = s0 + j < a.nsplit;
       const size_t slot = row0 + (size_t)(s0 + j) * a.rows_max;
       ml[j] = in ? a.ws_ml[slot] : make_float2(-INFINITY, 0.f);
-      v[j] = in ? *reinterpret_cast<const uint2*>(a.ws_o + slot * kD + dim) : make_uint2(0u, 0u);
+      v[j] = in ? *reinterpret_cast<const uint4*>(a.ws_o + slot * kD + dim) : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -694,26 +698,28 @@ __global__ __launch_bounds__(256) void verify_combine_kernel(const VerifyArgs a)
         const float m_new = fmaxf(M, ml[j].x);
         const float c = exp2f(M - m_new);   // 0 while nothing has been merged
         const float w = ml[j].y * exp2f(ml[j].x - m_new);
-        num.x = num.x * c + w * bf16_lo(v[j].x);
-        num.y = num.y * c + w * bf16_hi(v[j].x);
-        num.z = num.z * c + w * bf16_lo(v[j].y);
-        num.w = num.w * c + w * bf16_hi(v[j].y);
+        const uint32_t wv[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          num[2 * e] = num[2 * e] * c + w * bf16_lo(wv[e]);
+          num[2 * e + 1] = num[2 * e + 1] * c + w * bf16_hi(wv[e]);
+        }
         den = den * c + w;
         M = m_new;
       }
     }
   }
-  const int b = bg / a.Hkv;
-  const int g = bg - b * a.Hkv;
-  const int T = min(max(a.node_count[b], 0), a.T_max);
   if (qr >= T * a.G) return;
+  const int g = bg - b * a.Hkv;
   const int u = qr / a.G;
   const int h = g * a.G + (qr - u * a.G);
   const float inv = 1.f / den;
-  uint2 pk;
-  pk.x = f32_to_bf16_bits(num.x * inv) | (f32_to_bf16_bits(num.y * inv) << 16);
-  pk.y = f32_to_bf16_bits(num.z * inv) | (f32_to_bf16_bits(num.w * inv) << 16);
-  *reinterpret_cast<uint2*>(a.out + (((size_t)b * a.T_max + u) * a.Hq + h) * kD + dim) = pk;
+  uint4 pk;
+  pk.x = f32_to_bf16_bits(num[0] * inv) | (f32_to_bf16_bits(num[1] * inv) << 16);
+  pk.y = f32_to_bf16_bits(num[2] * inv) | (f32_to_bf16_bits(num[3] * inv) << 16);
+  pk.z = f32_to_bf16_bits(num[4] * inv) | (f32_to_bf16_bits(num[5] * inv) << 16);
+  pk.w = f32_to_bf16_bits(num[6] * inv) | (f32_to_bf16_bits(num[7] * inv) << 16);
+  *reinterpret_cast<uint4*>(a.out + (((size_t)b * a.T_max + u) * a.Hq + h) * kD + dim) = pk;
   if (dim == 0 && a.lse) a.lse[((size_t)b * a.Hq + h) * a.T_max + u] = (M + log2f(den)) * kLn2;
 }
 
@@ -811,7 +817,8 @@ hipError_t launch_tree_verify_attn(const uint16_t* q, const uint16_t* k_ctx, con
     hipLaunchKernelGGL((tree_verify_kernel<1, 8, 1, false>), grid, dim3(8 * kWave), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.nsplit == 1) return e;
-  hipLaunchKernelGGL(verify_combine_kernel, dim3((p.rows_max + 7) / 8, B * Hkv), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(verify_combine_kernel, dim3((p.rows_max + kCombineRows - 1) / kCombineRows, B * Hkv),
+                     dim3(kCombineRows * 16), 0, stream, a);
   return hipGetLastError();
 }
 
