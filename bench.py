@@ -30,9 +30,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "639a35c13f128425cb7d3cc6c3545beeb146127762b02ca30357d1c8580dcc76",
-    "fetch_kib": 276121.8,
-    "write_kib": 16567.6,
+    "source_sha256": "dbfc0dbcc747fd546d4922e532490fe0849bee5002874a0c1963533adbf74aa3",
+    "fetch_kib": 276119.8,
+    "write_kib": 16567.7,
     "fetch_scale": 2.0,
     "write_scale": 1.0,
 }
