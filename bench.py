@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "dbfc0dbcc747fd546d4922e532490fe0849bee5002874a0c1963533adbf74aa3",
+    "source_sha256": "f17da893b8446dae8f25586867d1cc1638314d885625da125e53389b2d5ecb2b",
     "fetch_kib": 276119.8,
     "write_kib": 16567.7,
     "fetch_scale": 2.0,

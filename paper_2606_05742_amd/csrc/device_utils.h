@@ -252,8 +252,9 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
 // The same load with the non-temporal hint, for data that one wave reads
 // once and nothing reads again (the semantic scan's bank rows): the caches
 // then treat it as streaming instead of keeping it.  The scan reads its rows
-// 11 % faster with it; the verify's tiles must not take it, since the second
-// row group of a (sequence, kv head) reads them from L2.
+// 11 % faster with it.  The verify kernel has its own scalar-base form and
+// uses it only when one workgroup reads each tile: with two or more row
+// groups of a (sequence, kv head), the later readers take the tiles from L2.
 __device__ __forceinline__ void dma16_stream(const void* gptr, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
                :
