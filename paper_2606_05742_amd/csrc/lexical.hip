@@ -10,7 +10,8 @@
 // {j : len(j) >= n*} in ascending order with a wave scan and a 16-entry
 // workgroup scan of the per-thread hit counts.  A context that fits one piece
 // is staged once and scanned once: the match lengths stay in registers
-// between the two steps.
+// between the two steps; when every row of the batch fits one piece, the
+// whole row is staged together with the length load.
 #include "adapld_internal.h"
 #include "device_utils.h"
 
@@ -176,6 +177,26 @@ __global__ __launch_bounds__(kLexThreads) void lexical_match_kernel(
   const int lane = lane_id();
   const int wave = tid / kWave;
   const int32_t* __restrict__ M = tokens + (size_t)b * L_stride;
+
+  // When every context fits one piece (L_stride <= kLexChunk + 1), the whole
+  // allocated row is staged without waiting for the length, so the length and
+  // the tokens arrive in one memory round trip, and the query suffix is read
+  // from the staged copy.
+  if (L_stride <= kLexChunk + 1 && n_max <= 15) {
+    const int L_raw = lens[b];
+    stage(M, s_tok, 0, 0, L_stride);
+    const int L = min(max(L_raw, 0), L_stride);
+    __syncthreads();
+    if (tid < n_max && tid < L) s_suffix[tid] = s_tok[kHalo + L - 1 - tid];
+    __syncthreads();
+    const int J = L - 1;
+    int32_t* __restrict__ out = cand_pos + (size_t)b * L_stride;
+    if (n_max <= 4) single_pass_nm<4>(s_tok, s_suffix, s_red, J, n_max, out, cand_count + b, match_n + b);
+    else if (n_max <= 8) single_pass_nm<8>(s_tok, s_suffix, s_red, J, n_max, out, cand_count + b, match_n + b);
+    else single_pass_nm<16>(s_tok, s_suffix, s_red, J, n_max, out, cand_count + b, match_n + b);
+    return;
+  }
+
   const int L = min(max(lens[b], 0), L_stride);
   const int J = L - 1;  // candidate end positions are [0, J)
 
