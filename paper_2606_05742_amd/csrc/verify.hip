@@ -740,7 +740,8 @@ VerifyPlan plan_verify(int B, int L_stride, int T_max, int Hq, int Hkv) {
   constexpr double kCombineTiles = 6.0;   // the combine launch and its traffic
   // With more than one row group, every tile goes to LDS once per row group
   // (the second from L2) and must stay in L2 for it; with one row group the
-  // tiles stream once, non-temporally (measured: 4 % faster at C3).
+  // tiles stream once, non-temporally (measured 4 % faster on 16 sequences of
+  // 8192 keys with 32 query heads over 8 and 52-node trees).
   constexpr double kSharedTile = 0.1;
   struct Cand { int waves, kh; double per_tile; };   // per_tile: SIMD cost of one 64-key tile
   const Cand cands[] = {{8, 1, 2.0}, {8, 2, 1.0}};
