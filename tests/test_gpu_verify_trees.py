@@ -10,7 +10,8 @@ shapes take the other decompositions: 40 query heads over 8 with T_max = 137
 (every wave its own block, three row groups), 64 over 8 with T_max = 72 and
 a split context (five row groups, two splits), and 32 heads without
 grouping (one row group, four splits); two cases at 8192 keys take
-whole-workgroup row blocks in one row group with four and eight splits;
+whole-workgroup row blocks in one row group with four and eight splits,
+and one whole-workgroup row blocks in five row groups with three splits;
 the last case is the largest tree the
 boundary takes (256 nodes)."""
 import math
@@ -132,6 +133,15 @@ def test_random_trees_eight_splits():
     counts = [52, 40, 1, 52]
     lens = [8192, 8000, 64, 1000]
     run_case(8192, lens, counts, seed=9, B=4, HQ=32, HKV=8, T_MAX=52, plan_is=(1, 1, 8))
+
+
+def test_random_trees_row_groups_and_odd_splits():
+    """64 query heads over 8 with T_max = 137: whole-workgroup row blocks in
+    five row groups (L2-shared tiles) and the context in three splits, the
+    second sequence's context ending inside the second split."""
+    counts = [137, 90]
+    lens = [1500, 700]
+    run_case(1500, lens, counts, seed=10, B=2, HQ=64, HKV=8, T_MAX=137, plan_is=(1, 5, 3))
 
 
 def test_random_trees_no_grouping():
