@@ -676,10 +676,11 @@ __global__ __launch_bounds__(kCombineRows * 16) void verify_combine_kernel(const
   const int b = bg / a.Hkv;
   const int T = min(max(a.node_count[b], 0), a.T_max);
   // One pass over the splits in index order, four at a time.  The maxima and
-  // partials of a group are loaded together, and before node_count is known
-  // (every slot is in bounds), so a call with up to four splits costs one
-  // memory round trip; the running max moves online.  Split s carries O_s/l_s
-  // with weight l_s 2^(m_s - M).
+  // partials of a group are loaded together, and with node_count rather than
+  // after it (every slot is in bounds; rows past the tree are dropped at the
+  // end), so a call with up to four splits costs one memory round trip; the
+  // running max moves online.  Split s carries O_s/l_s with weight
+  // l_s 2^(m_s - M).
   float M = -INFINITY, den = 0.f;
   float num[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < a.nsplit; s0 += 4) {
