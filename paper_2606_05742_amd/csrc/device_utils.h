@@ -227,6 +227,17 @@ __device__ __forceinline__ uint64_t bitonic_steps(uint64_t v) {
   else return v;
 }
 __device__ __forceinline__ uint64_t bitonic_sort_desc(uint64_t v) { return bitonic_steps<2, 1>(v); }
+template <int K, int J>
+__device__ __forceinline__ uint32_t bitonic_steps_u32(uint32_t v) {
+  const int lane = lane_id();
+  const uint32_t p = xor_lanes_u32<J>(v);
+  const bool keep_max = ((lane & J) == 0) == ((lane & K) == 0);
+  v = keep_max ? (v > p ? v : p) : (v < p ? v : p);
+  if constexpr (J > 1) return bitonic_steps_u32<K, J / 2>(v);
+  else if constexpr (K < kWave) return bitonic_steps_u32<2 * K, K>(v);
+  else return v;
+}
+__device__ __forceinline__ uint32_t bitonic_sort_desc_u32(uint32_t v) { return bitonic_steps_u32<2, 1>(v); }
 
 // s_waitcnt vmcnt(n) (gfx9 encoding, n < 64); lgkmcnt and expcnt unconstrained.
 template <int N>

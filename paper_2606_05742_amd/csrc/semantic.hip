@@ -368,8 +368,11 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
   }
   th = wave_max_u64(th);
   if (wave == 0 && nvalid >= k) {
-    y = bitonic_sort_desc(y);
-    const uint64_t thb = readlane_u64(y, k - 1);
+    // The bound needs only the score word: at least k heads have a score word
+    // at or above the k-th largest one, so at least k keys reach it with a
+    // zero position word.  Sorting 32-bit words halves the lane exchanges.
+    const uint32_t ys = bitonic_sort_desc_u32((uint32_t)(y >> 32));
+    const uint64_t thb = (uint64_t)(uint32_t)__builtin_amdgcn_readlane(ys, k - 1) << 32;
     th = thb > th ? thb : th;
   }
   if (lane == 0) s_red[wave] = th;
@@ -408,7 +411,8 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
   if (ncand <= kMaxCand) {
     for (int base = 0; base < ncand; base += kWave) {
       const uint64_t v = base + lane < ncand ? s_cand[base + lane] : 0ull;
-      mine = topk_merge(mine, bitonic_sort_desc(v));
+      const uint64_t sorted = bitonic_sort_desc(v);
+      mine = base == 0 ? sorted : topk_merge(mine, sorted);   // the first batch needs no merge
     }
   } else {
     for (int c = 0; c < nvalid; ++c) {
