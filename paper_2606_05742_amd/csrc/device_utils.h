@@ -216,17 +216,22 @@ __device__ __forceinline__ uint64_t topk_merge(uint64_t mine, uint64_t other) {
 
 // Sort a wave-wide list of 64 keys descending (bitonic network): stage K
 // merges blocks of K, step J compares lanes J apart.
-template <int K, int J>
+template <int K, int J, int KMAX = kWave>
 __device__ __forceinline__ uint64_t bitonic_steps(uint64_t v) {
   const int lane = lane_id();
   const uint64_t p = xor_lanes_u64<J>(v);
   const bool keep_max = ((lane & J) == 0) == ((lane & K) == 0);
   v = keep_max ? (v > p ? v : p) : (v < p ? v : p);
-  if constexpr (J > 1) return bitonic_steps<K, J / 2>(v);
-  else if constexpr (K < kWave) return bitonic_steps<2 * K, K>(v);
+  if constexpr (J > 1) return bitonic_steps<K, J / 2, KMAX>(v);
+  else if constexpr (K < KMAX) return bitonic_steps<2 * K, K, KMAX>(v);
   else return v;
 }
 __device__ __forceinline__ uint64_t bitonic_sort_desc(uint64_t v) { return bitonic_steps<2, 1>(v); }
+// The same when only lanes below N (16 or 32) hold keys and the rest hold 0:
+// sorting each block of N lanes leaves block 0 descending and the rest zero,
+// the result of the full sort, in fewer steps (10 or 15 instead of 21).
+template <int N>
+__device__ __forceinline__ uint64_t bitonic_sort_desc_first(uint64_t v) { return bitonic_steps<2, 1, N>(v); }
 template <int K, int J>
 __device__ __forceinline__ uint32_t bitonic_steps_u32(uint32_t v) {
   const int lane = lane_id();

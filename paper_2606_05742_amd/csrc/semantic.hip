@@ -411,7 +411,9 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
   if (ncand <= kMaxCand) {
     for (int base = 0; base < ncand; base += kWave) {
       const uint64_t v = base + lane < ncand ? s_cand[base + lane] : 0ull;
-      const uint64_t sorted = bitonic_sort_desc(v);
+      const int n = ncand - base;   // keys in this batch (lanes below n)
+      const uint64_t sorted = n <= 16 ? bitonic_sort_desc_first<16>(v)
+                              : n <= 32 ? bitonic_sort_desc_first<32>(v) : bitonic_sort_desc(v);
       mine = base == 0 ? sorted : topk_merge(mine, sorted);   // the first batch needs no merge
     }
   } else {
