@@ -307,7 +307,7 @@ __global__ __launch_bounds__(kScanThreads) void topk_merge_kernel(const ScanArgs
                                                                   int32_t* __restrict__ kind,
                                                                   const TreeOut tree) {
   __shared__ uint64_t s_cand[kMaxCand];
-  __shared__ int s_start[2 * ADAPLD_MAX_TREE_NODES];
+  __shared__ __attribute__((aligned(8))) int s_start[2 * ADAPLD_MAX_TREE_NODES];
   __shared__ uint64_t s_red[kScanWaves];
   __shared__ int s_sum[kScanWaves][2];
   __shared__ int s_ncand;

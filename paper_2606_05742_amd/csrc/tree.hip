@@ -15,7 +15,7 @@ __global__ __launch_bounds__(kWave) void build_draft_tree_kernel(
     int32_t* __restrict__ node_token, int32_t* __restrict__ node_parent,
     int32_t* __restrict__ node_depth, int32_t* __restrict__ node_src,
     int32_t* __restrict__ node_count, uint64_t* __restrict__ tree_mask) {
-  __shared__ int s_start[2 * ADAPLD_MAX_TREE_NODES];
+  __shared__ __attribute__((aligned(8))) int s_start[2 * ADAPLD_MAX_TREE_NODES];
   const int b = blockIdx.x;
   const int lane = lane_id();
   const int L = min(max(lens[b], 0), L_stride);

@@ -19,7 +19,8 @@ namespace adapld {
 
 
 // Called by every lane of one wave; s_start holds 2 * ADAPLD_MAX_TREE_NODES
-// ints of LDS that only this wave uses.
+// ints of LDS, 8-byte aligned, that only this wave uses (node u's branch
+// start and source row as a pair).
 __device__ __forceinline__ void build_tree_wave(const TreeOut& t, int b, int L_stride, int L, int r, int cnt,
                                                 int* s_start) {
   const int lane = lane_id();
@@ -27,12 +28,20 @@ __device__ __forceinline__ void build_tree_wave(const TreeOut& t, int b, int L_s
   int tok = -1;
   const bool valid = lane < cnt && r >= 0 && r <= L - 2;
   if (valid) tok = M[r + 1];
-  // A lane is a new branch if no lower valid lane holds the same successor token.
+  // A lane is a new branch if no lower valid lane holds the same successor
+  // token.  The tokens and validity of 8 lanes at a time are read as scalars
+  // together (independent reads, not one dependent read per lane); lanes at
+  // or past cnt are never valid.
   bool dup = false;
-  for (int j = 0; j < cnt; ++j) {   // lane j's token and validity as scalars
-    const int tj = __builtin_amdgcn_readlane(tok, j);
-    const int vj = __builtin_amdgcn_readlane((int)valid, j);
-    dup |= (j < lane) && vj && tj == tok;
+  for (int j0 = 0; j0 < cnt; j0 += 8) {
+    int tj[8], vj[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      tj[i] = __builtin_amdgcn_readlane(tok, min(j0 + i, kWave - 1));
+      vj[i] = __builtin_amdgcn_readlane((int)valid, min(j0 + i, kWave - 1));
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) dup |= (j0 + i < lane) && vj[i] && tj[i] == tok;
   }
   const bool opens = valid && !dup;
   const int branch = __popcll(__ballot(opens) & lanes_below());
@@ -45,17 +54,14 @@ __device__ __forceinline__ void build_tree_wave(const TreeOut& t, int b, int L_s
   const int T = __builtin_amdgcn_readlane(incl, kWave - 1);
 
   const size_t nb = (size_t)b * t.T_max;
-  // Every node's branch start and source row go to LDS; the nodes are then
-  // written 64 at a time across the lanes, with the token loads of all of
-  // them in flight together (a lane walking its own branch would wait for
-  // each token, and for its earlier stores, in turn).
-  int* s_row = s_start + ADAPLD_MAX_TREE_NODES;
-  for (int dd = 0; dd < len; ++dd) {
-    s_start[start + dd] = start;
-    s_row[start + dd] = r;
-  }
+  // Every node's branch start and source row go to LDS as one pair; the
+  // nodes are then written 64 at a time across the lanes, with the token
+  // loads of all of them in flight together (a lane walking its own branch
+  // would wait for each token, and for its earlier stores, in turn).
+  int2* s_pair = reinterpret_cast<int2*>(s_start);
+  for (int dd = 0; dd < len; ++dd) s_pair[start + dd] = make_int2(start, r);
   if (lane == 0) t.node_count[b] = T;
-  // s_start and s_row are written and read by this wave only; its LDS
+  // The pairs are written and read by this wave only; its LDS
   // operations complete in order, so a wave-level fence is enough.
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -65,9 +71,11 @@ __device__ __forceinline__ void build_tree_wave(const TreeOut& t, int b, int L_s
     int tok_u[kChunks], src_u[kChunks], dd_u[kChunks];
 #pragma unroll
     for (int c = 0; c < kChunks; ++c) {
+      if (c * kWave >= T) break;                      // wave-uniform
       const int u = min(c * kWave + lane, T - 1);   // past T: a repeat of node T-1, not stored
-      dd_u[c] = u - s_start[u];
-      src_u[c] = s_row[u] + 1 + dd_u[c];             // <= L-1 by the branch length
+      const int2 pr = s_pair[u];
+      dd_u[c] = u - pr.x;
+      src_u[c] = pr.y + 1 + dd_u[c];                 // <= L-1 by the branch length
       tok_u[c] = M[src_u[c]];
     }
 #pragma unroll
@@ -89,7 +97,7 @@ __device__ __forceinline__ void build_tree_wave(const TreeOut& t, int b, int L_s
     const int w = idx - u * nw;
     uint64_t bits = 0;
     if (u < T) {
-      const int lo = max(s_start[u], 64 * w);
+      const int lo = max(s_pair[u].x, 64 * w);
       const int hi = min(u, 64 * w + 63);  // inclusive
       if (lo <= hi) {
         const int n = hi - lo + 1;
