@@ -81,14 +81,15 @@ __device__ __forceinline__ int suffix_len(const int* s_tok, int p0, const int* s
 // [tid * per, +per); per is odd, so the 64 lanes of a wave, reading word
 // tid * per + i at the same time, touch 64 different LDS banks.
 //
-// The match lengths need no data-dependent loop: the run's tokens and the
-// NM - 1 before it are read from LDS into registers once, and the length at j
-// is the number of trailing ones of the mask of k < NM with
-// M[j - k] == M[L - 1 - k], capped at min(n_max, j + 1) (so tokens before
-// position 0, and suffix entries past the cap, never count).  They stay in
+// The length at j is the number of k < min(n_max, j + 1) from 0 up with
+// M[j - k] == M[L - 1 - k] (so tokens before position 0 never count).  It is
+// 0 unless M[j] is the query's last token, so one compare per position picks
+// out the few positions that need more, and only those read the tokens before
+// them (16 waves on one CU make this VALU-bound: a full compare chain for
+// every position cost about three times as long).  Runs of 33 positions
+// keep the full chain, which measured faster there.  The lengths stay in
 // registers (4 bits each) for the ordered compaction after the workgroup
-// reduction of n*.  NM and PMAX are compile-time bounds, so every register
-// index is a constant.
+// reduction of n*; NM and PMAX are compile-time bounds.
 template <int NM, int PMAX>
 __device__ __forceinline__ void single_pass(const int* s_tok, const int* s_suffix, int* s_red, int J, int per,
                                             int n_max, int32_t* __restrict__ out, int32_t* __restrict__ cand_count,
@@ -97,24 +98,52 @@ __device__ __forceinline__ void single_pass(const int* s_tok, const int* s_suffi
   const int lane = lane_id();
   const int wave = tid / kWave;
   const int q0 = tid * per;
-  int suf[NM];
-#pragma unroll
-  for (int k = 0; k < NM; ++k) suf[k] = k < n_max ? s_suffix[k] : 0;
-  int w[NM - 1 + PMAX];   // w[i] = M[q0 - (NM - 1) + i]
-#pragma unroll
-  for (int i = 0; i < NM - 1 + PMAX; ++i) w[i] = i < NM - 1 + per ? s_tok[kHalo + q0 - (NM - 1) + i] : 0;
   uint64_t lens4[(PMAX + 15) / 16] = {};
   int best = 0;
+  if constexpr (PMAX <= 17) {
+    // Only positions whose token is the query's last token have a match length
+    // of 1 or more; one compare per position finds them, and their lengths are
+    // then extended against the rest of the suffix (capped at
+    // min(n_max, j + 1)) from LDS.  Every other position keeps length 0.
+    const int s0 = s_suffix[0];
+    uint64_t m0 = 0;
 #pragma unroll
-  for (int e = 0; e < PMAX; ++e) {
-    const int j = q0 + e;
-    if (e < per && j < J) {
-      uint32_t eq = 0;
+    for (int e = 0; e < PMAX; ++e)
+      if (e < per && q0 + e < J && s_tok[kHalo + q0 + e] == s0) m0 |= 1ull << e;
+    for (uint64_t rem = m0; rem; rem &= rem - 1) {
+      const int e = __builtin_ctzll(rem);
+      const int j = q0 + e;
+      const int cap = min(min(n_max, NM), j + 1);
+      int n = 1;
+      while (n < cap && s_tok[kHalo + j - n] == s_suffix[n]) ++n;
+      const uint64_t bits = (uint64_t)n << (4 * (e & 15));
 #pragma unroll
-      for (int k = 0; k < NM; ++k) eq |= (uint32_t)(w[e + NM - 1 - k] == suf[k]) << k;
-      const int n = min(__builtin_ctz(~eq), min(n_max, j + 1));
-      lens4[e >> 4] |= (uint64_t)n << (4 * (e & 15));
+      for (int w = 0; w < (PMAX + 15) / 16; ++w)
+        if ((e >> 4) == w) lens4[w] |= bits;
       best = max(best, n);
+    }
+  } else {
+    // Runs of up to 33 positions (contexts beyond 16 Ki tokens): the
+    // first-token filter's per-match loop costs more than it saves there, so
+    // every position takes the full compare chain against the suffix held in
+    // registers, with the run's tokens and the NM - 1 before it.
+    int suf[NM];
+#pragma unroll
+    for (int k = 0; k < NM; ++k) suf[k] = k < n_max ? s_suffix[k] : 0;
+    int w[NM - 1 + PMAX];   // w[i] = M[q0 - (NM - 1) + i]
+#pragma unroll
+    for (int i = 0; i < NM - 1 + PMAX; ++i) w[i] = i < NM - 1 + per ? s_tok[kHalo + q0 - (NM - 1) + i] : 0;
+#pragma unroll
+    for (int e = 0; e < PMAX; ++e) {
+      const int j = q0 + e;
+      if (e < per && j < J) {
+        uint32_t eq = 0;
+#pragma unroll
+        for (int k = 0; k < NM; ++k) eq |= (uint32_t)(w[e + NM - 1 - k] == suf[k]) << k;
+        const int n = min(__builtin_ctz(~eq), min(n_max, j + 1));
+        lens4[e >> 4] |= (uint64_t)n << (4 * (e & 15));
+        best = max(best, n);
+      }
     }
   }
   best = wave_max_i32(best);
