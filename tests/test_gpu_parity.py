@@ -189,6 +189,34 @@ def test_lexical_long_contexts(n_max):
     assert int(mn[0]) == min(n_max, 40) and int(mn[2]) == min(n_max, 40)
 
 
+@pytest.mark.parametrize("L", [5000, 70000])
+def test_lexical_nmax_at_limit(L):
+    """n_max = 64, the largest the boundary takes: a planted 70-token repeat
+    gives n* = 64 (the cap), a 63-token one at least 63, and in contexts of
+    more than one LDS piece (32768 tokens) a 64-token repeat straddles the
+    piece boundary."""
+    cfg = small_config(B=3, L=L, d=8, n_max=64, seed=98, V=60, copy_frac=0.5, span=(8, 64))
+    x = make_inputs(cfg, with_bank=False, with_verify=False)
+    t = x["tokens"]
+    x["lens"][:] = [L, L - 301, L // 2 + 5]
+    plants = ((0, 70, 1000), (1, 63, L // 2 - 40), (2, 64, 32768 - 30 if L // 2 > 32768 + 64 else L // 4))
+    t[0, 3000:3070] = t[0, 1000:1070]   # a second full-length occurrence in sequence 0
+    for b, n, src in plants:
+        Lb = int(x["lens"][b])
+        t[b, Lb - n:Lb] = t[b, src:src + n]
+    lens = dev_i32(x["lens"])
+    cp, cc, mn = adapld.lexical_match(dev_i32(t), lens, 64)
+    torch.cuda.synchronize()
+    cp, cc, mn = cp.cpu().numpy(), cc.cpu().numpy(), mn.cpu().numpy()
+    for b, n, _ in plants:
+        Lb = int(x["lens"][b])
+        n_o, C = oracle.lexical_match(t[b, :Lb], 64)
+        assert n_o >= min(n, 64)
+        assert int(mn[b]) == n_o and int(cc[b]) == len(C), (b, int(mn[b]), n_o, int(cc[b]), len(C))
+        np.testing.assert_array_equal(cp[b, :len(C)], C)
+    assert int(mn[0]) == 64 and int(cc[0]) >= 2 and int(mn[2]) == 64
+
+
 @pytest.mark.parametrize("L,n_max", [(9217, 4), (9300, 7), (17500, 13), (32769, 4), (32769, 15)])
 def test_lexical_single_piece_runs(L, n_max):
     """Contexts of one LDS piece at the edges of the single pass's run-length
